@@ -1,0 +1,216 @@
+"""Pins of the Direct-P oracle (oracle/directp.py): closed forms, invariants,
+special cases that reduce to textbook attention, and the paper's error band."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import directp, e2m1, exact, mxfp4
+
+SCALE64 = 0.125  # 1/sqrt(64)
+
+
+def _golden(golden_dir, name, key):
+    with open(os.path.join(golden_dir, name)) as f:
+        for line in f:
+            if line.startswith(key + " "):
+                return [float(t) for t in line.split()[1:]]
+    raise KeyError(key)
+
+
+def _quantized_head(rng, N, d, scale_q=1.0):
+    q = rng.standard_normal((N, d)) * scale_q
+    k = rng.standard_normal((N, d))
+    v = rng.standard_normal((N, d))
+    ops = mxfp4.quantize(q) + mxfp4.quantize(k) + mxfp4.quantize(v, axis=-2)
+    return (q, k, v), ops
+
+
+def _raw_for_x(xs, softmax_scale, mode):
+    """A 32-score block whose maximum has y = 0.5 (E_B = 0) and whose other scores
+    have x = y - E_B + log2 6 equal to ``xs``."""
+    y = np.concatenate([[0.5], np.asarray(xs) - directp.LOG2_6])
+    raw = y / (softmax_scale / 36.0 * directp.LOG2_E)
+    if mode == "affine32":
+        c_y, _, _ = directp.fp32_coefficients(softmax_scale, 1.5, 1.2)
+        raw = (y / np.float64(c_y)).astype(np.float32).astype(np.float64)
+    return np.pad(raw, (0, 32 - len(raw)), constant_values=raw[1])[None, :]
+
+
+@pytest.mark.parametrize("mode,eps", [("affine64", 1e-9), ("affine32", 1e-4)])
+@pytest.mark.parametrize("ab_key", ["fast_affine", "wan_affine"])
+def test_code_boundaries_closed_form(golden_dir, mode, eps, ab_key):
+    """Codes change exactly at x_j = (t_j - B) / A (eq. affine-log-boundaries)."""
+    A, B = _golden(golden_dir, "e2m1.txt", ab_key)
+    t = _golden(golden_dir, "e2m1.txt", "boundaries")
+    # A and B travel as fp32 arguments; the boundaries follow the rounded values
+    xj = (np.array(t) - float(np.float32(B))) / float(np.float32(A))
+    for j, x in enumerate(xj):
+        raw = _raw_for_x([x - eps, x + eps], SCALE64, mode)
+        E, _, k = directp.block_exponents_and_codes(raw, SCALE64, A, B, mode)
+        assert E[0, 0] == 0
+        assert k[0, 1] == j and k[0, 2] == j + 1, (j, x, k[0, :3])
+    if ab_key == "fast_affine":
+        # the printed (A, B) = (1.5, 1.2) give these boundaries
+        assert np.allclose(xj, [-0.63333, -0.3, 0.03333, 0.36667, 0.86667, 1.53333, 2.53333], atol=1e-5)
+
+
+@pytest.mark.parametrize("mode", ["affine32", "affine64", "exp2"])
+def test_block_argmax_gets_code_six(mode):
+    rng = np.random.default_rng(10)
+    raw = (rng.standard_normal((64, 256)) * 300).astype(np.float32).astype(np.float64)
+    E, q, k = directp.block_exponents_and_codes(raw, SCALE64, 1.5, 1.2, mode)
+    blocks = k.reshape(64, 8, 32)
+    arg = raw.reshape(64, 8, 32).argmax(axis=-1)
+    assert np.all(np.take_along_axis(blocks, arg[..., None], axis=-1) == 7)
+    # and every other code is at most that
+    assert blocks.max() == 7
+
+
+@pytest.mark.parametrize("mode", ["affine64", "exp2", "exp2_exact"])
+def test_codes_invariant_under_integer_log2_shift(mode):
+    rng = np.random.default_rng(11)
+    raw = rng.standard_normal((32, 256)) * 200
+    per_unit = 36.0 / (SCALE64 * directp.LOG2_E)   # raw increment that moves y by one
+    for shift in (-7, 3, 40):
+        E0, q0, _ = directp.block_exponents_and_codes(raw, SCALE64, 1.5, 1.2, mode)
+        E1, q1, _ = directp.block_exponents_and_codes(raw + shift * per_unit, SCALE64, 1.5, 1.2, mode)
+        assert np.array_equal(E1, E0 + shift)
+        if mode == "exp2_exact":
+            assert np.allclose(q0, q1, rtol=1e-9, atol=0)
+        else:
+            assert np.array_equal(q0, q1)
+
+
+def test_fp32_decision_agrees_with_fp64_formula():
+    rng = np.random.default_rng(12)
+    (_, _, _), ops = _quantized_head(rng, 512, 128)
+    q6 = mxfp4.scaled_operand(*ops[0:2])
+    k6 = mxfp4.scaled_operand(*ops[2:4])
+    raw = directp.raw_scores(q6, k6)
+    s = 1 / np.sqrt(128)
+    E32, _, k32 = directp.block_exponents_and_codes(raw, s, 1.5, 1.2, "affine32")
+    E64, _, k64 = directp.block_exponents_and_codes(raw, s, 1.5, 1.2, "affine64")
+    assert np.mean(E32 != E64) < 1e-4
+    assert np.mean(k32 != k64) < 1e-4
+
+
+@pytest.mark.parametrize("mode", ["affine32", "exp2"])
+def test_represented_probabilities_sum_to_one(mode):
+    rng = np.random.default_rng(13)
+    _, ops = _quantized_head(rng, 256, 64, scale_q=3.0)
+    res = directp.forward_rows(*ops, np.arange(256), SCALE64, mode=mode)
+    p = directp.represented_probabilities(res["E"], e2m1.MAGNITUDES[res["codes"]], res["M"])
+    assert np.allclose(p.sum(axis=1), 1.0, rtol=0, atol=1e-13)
+    # the denominator is the same weighted code sum
+    w = np.ldexp(1.0, res["E"] - res["M"][:, None])
+    c = e2m1.MAGNITUDES[res["codes"]].reshape(256, -1, 32).sum(axis=-1)
+    assert np.allclose(res["D"], (w * c).sum(axis=1), rtol=1e-15)
+
+
+@pytest.mark.parametrize("tile", [32, 64, 128, 512])
+def test_online_equals_whole_row(tile):
+    rng = np.random.default_rng(14)
+    _, ops = _quantized_head(rng, 512, 64, scale_q=4.0)   # peaked rows: the reference moves
+    rows = np.arange(0, 512, 3)
+    brute = directp.forward_rows(*ops, rows, SCALE64)
+    online = directp.forward_rows_online(*ops, rows, SCALE64, tile=tile)
+    assert np.array_equal(brute["codes"], online["codes"])
+    assert np.array_equal(brute["E"], online["E"])
+    assert np.array_equal(brute["M"], online["M"])
+    assert np.allclose(online["O"], brute["O"], rtol=0, atol=1e-12 * np.abs(brute["O"]).max())
+    assert np.allclose(online["D"], brute["D"], rtol=1e-13)
+
+
+def test_zero_queries_give_uniform_p_and_mean_value():
+    """Q = 0: y = 0, E_B = 0, u = A log2 6 + B = 5.08 -> every code is 6."""
+    rng = np.random.default_rng(15)
+    N, d = 256, 64
+    v = rng.standard_normal((N, d))
+    ops = mxfp4.quantize(np.zeros((N, d))) + mxfp4.quantize(rng.standard_normal((N, d))) \
+        + mxfp4.quantize(v, axis=-2)
+    res = directp.forward_rows(*ops, np.arange(N), SCALE64)
+    assert np.all(res["codes"] == 7) and np.all(res["E"] == 0)
+    vhat = mxfp4.dequantize(*ops[4:6]).T
+    assert np.allclose(res["O"], vhat.mean(axis=0)[None, :], rtol=0, atol=1e-14)
+
+
+def test_constant_power_of_two_values_pass_through():
+    rng = np.random.default_rng(16)
+    N, d = 256, 64
+    for k in (-3, 0, 5):
+        ops = mxfp4.quantize(rng.standard_normal((N, d)) * 2) + mxfp4.quantize(rng.standard_normal((N, d))) \
+            + mxfp4.quantize(np.full((N, d), 2.0 ** k), axis=-2)
+        res = directp.forward_rows(*ops, np.arange(N), SCALE64)
+        assert np.all(res["O"] == 2.0 ** k)
+
+
+def test_unrounded_exp2_reduces_to_softmax_attention():
+    """Without E2M1 rounding, p = 2**x = 6 * 2**(y - E_B) and the weights
+    2**(E_B - M) make the output exactly softmax attention over Qhat, Khat, Vhat."""
+    rng = np.random.default_rng(17)
+    N, d = 384, 64
+    _, ops = _quantized_head(rng, N, d, scale_q=2.0)
+    res = directp.forward_rows(*ops, np.arange(N), SCALE64, mode="exp2_exact")
+    qh = mxfp4.dequantize(*ops[0:2])
+    kh = mxfp4.dequantize(*ops[2:4])
+    vh = mxfp4.dequantize(*ops[4:6]).T
+    ref = exact.attention(qh, kh, vh, SCALE64)
+    assert np.allclose(res["O"], ref, rtol=0, atol=1e-12)
+
+
+def test_dominant_key_selects_its_value():
+    rng = np.random.default_rng(18)
+    N, d, jstar = 256, 64, 77
+    k = rng.standard_normal((N, d))
+    k[jstar] = 4.0
+    q = np.full((4, d), 4.0)
+    v = rng.standard_normal((N, d))
+    ops = mxfp4.quantize(q) + mxfp4.quantize(k) + mxfp4.quantize(v, axis=-2)
+    res = directp.forward_rows(*ops, np.arange(4), SCALE64)
+    vhat = mxfp4.dequantize(*ops[4:6]).T
+    assert np.allclose(res["O"], vhat[jstar][None, :], rtol=0, atol=1e-15)
+    # the dominant key's block sits more than 130 binades above every other block
+    others = np.delete(res["E"], jstar // 32, axis=1)
+    assert np.all(res["M"][:, None] - others > 130)
+
+
+def test_extreme_row_range_stays_finite():
+    rng = np.random.default_rng(19)
+    N, d = 512, 128
+    q = rng.standard_normal((N, d))
+    k = rng.standard_normal((N, d))
+    q[:, :3] *= 40.0
+    k[:, :3] *= 40.0
+    ops = mxfp4.quantize(q) + mxfp4.quantize(k) + mxfp4.quantize(rng.standard_normal((N, d)), axis=-2)
+    res = directp.forward_rows(*ops, np.arange(0, N, 7), 1 / np.sqrt(d))
+    span = res["E"].max(axis=1) - res["E"].min(axis=1)
+    assert span.max() > 254          # beyond the E8M0 byte range
+    assert np.all(np.isfinite(res["O"])) and np.all(res["D"] > 0)
+    u = directp.p_scale_bytes(res["E"], res["M"])
+    assert np.all(u[res["E"] - res["M"][:, None] < -127] == 0)
+
+
+def test_plausibility_band_against_exact_attention(golden_dir):
+    """MX/MX Direct-P fast on Gaussian D128 inputs lands near the paper's MX/MX
+    control (Table all-formats); the band is the paper's error scale, not parity."""
+    rng = np.random.default_rng(20)
+    N, d = 1024, 128
+    (q, k, v), ops = _quantized_head(rng, N, d)
+    s = 1 / np.sqrt(d)
+    res = directp.forward_rows(*ops, np.arange(N), s, want_codes=False)
+    ref = exact.attention(q, k, v, s)
+    cos, rel, _ = exact.error_metrics(res["O"], ref)
+    p_cos, p_rel = _golden(golden_dir, "operator_error.txt", "mxmx_s1024")
+    assert 0.90 <= cos <= 0.97 and 0.30 <= rel <= 0.42, (cos, rel)
+    assert abs(cos - p_cos) < 0.02 and abs(rel - p_rel) < 0.04, (cos, rel)
+    # the ideal converter is more accurate than the affine fit
+    ideal = directp.forward_rows(*ops, np.arange(N), s, mode="exp2", want_codes=False)
+    assert exact.error_metrics(ideal["O"], ref)[1] < rel
+
+
+def test_raw_scores_exactness_guard():
+    q6 = np.array([[1.0, 2.0 ** 40]])
+    k6 = np.array([[1.0, 2.0 ** -10]])
+    with pytest.raises(ValueError):
+        directp.raw_scores(q6, k6)   # 1 + 2**30 needs 31 significant bits
