@@ -1,0 +1,217 @@
+"""Throughput of the Direct-P full-MXFP4 attention forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is one forward pass (QK on scaled FP4 matrix cores, Direct-P, PV, the
+epilogue) over the whole workload with MXFP4 operands already resident in HBM;
+the paper times the attention kernel on prequantized operands and excludes
+quantization (its Sec. "Timed scope and operand contract").  The quantizer is
+timed separately and reported in the same line.  The metric is the paper's
+ops count 4 B H N^2 d per step (eq. hao-flops) over the step time.
+
+Prints one JSON line.  Also reported: the same-design BF16 kernel on the same
+inputs (windows interleaved with the FP4 ones, the paper's speedup
+t_BF16 / t_FP4), the roofline of the forward kernel against the dense MXFP4
+matrix peak, and the CPU oracle timed on a bounded sample of rows.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+MXFP4_PEAK_TFLOPS = 10100.0   # MI355X dense FP4/FP6 matrix peak
+BF16_PEAK_TFLOPS = 2500.0     # MI355X dense BF16 matrix peak
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_mxfp4_long_b1h32_n16384_d128_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_04105_amd", "csrc", "fwd_mxfp4.hip")
+
+
+def _source_sha():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _traffic():
+    """HBM bytes per forward launch from committed rocprofv3 counters, if they
+    were taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != _source_sha():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def _time_windows(torch, fns, steps, windows):
+    """Median per-call ms of each fn over ``windows`` interleaved windows of ``steps`` calls,
+    timed with events on the current stream (the stream the kernels are launched on)."""
+    res = {k: [] for k in fns}
+    for _ in range(windows):
+        for name, fn in fns.items():
+            start = torch.cuda.Event(enable_timing=True)
+            end = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            start.record()
+            for _ in range(steps):
+                fn()
+            end.record()
+            torch.cuda.synchronize()
+            res[name].append(start.elapsed_time(end) / steps)
+    return {k: sorted(v)[len(v) // 2] for k, v in res.items()}, res
+
+
+def cpu_oracle_baseline(w, budget_s=12.0):
+    """Time the oracle (as it stands) on consecutive rows of head (0, 0) until the budget is spent."""
+    import numpy as np
+    import workloads
+    from oracle import directp, mxfp4
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # threadpoolctl missing: report the affinity set
+        threads = len(os.sched_getaffinity(0))
+    q, k, v = workloads.generate(w, B=1, H=1)
+    q64, k64, v64 = (workloads.as_f64(t)[0, 0] for t in (q, k, v))
+    t0 = time.perf_counter()
+    kc, ks = mxfp4.quantize(k64, axis=-1)
+    vc, vs = mxfp4.quantize(v64, axis=-2)
+    rows_done = 0
+    chunk = 128
+    while rows_done < w.N and time.perf_counter() - t0 < budget_s:
+        qc, qs = mxfp4.quantize(q64[rows_done:rows_done + chunk], axis=-1)
+        directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(chunk), w.softmax_scale, want_codes=False)
+        rows_done += chunk
+    dt = time.perf_counter() - t0
+    flops = 4.0 * rows_done * w.N * w.d
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{rows_done} query rows of head (b0,h0) of {w.name} (all {w.N} keys), "
+                  f"including the oracle's own MXFP4 quantization of that head's K and V; {dt:.1f} s",
+        "seconds": round(dt, 2),
+        "full_workload_estimate_s": round(dt * w.rows / rows_done, 1),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--windows", type=int, default=5, help="interleaved FP4/BF16 timing windows")
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bf16", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the forward shards over (batch, head) with no communication "
+              "and nothing here uses a second GPU; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads
+    import paper_2609_04105_amd as fa
+
+    name = args.workload or workloads.BENCH_WORKLOAD
+    w = workloads.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    q, k, v = (t.to(dev) for t in workloads.generate(w))
+    torch.cuda.synchronize()
+
+    ops = fa.quantize_qkv(q, k, v)
+    out = torch.empty((w.B, w.H, w.N, w.d), dtype=torch.float32, device=dev)
+    q16, k16 = q.to(torch.bfloat16), k.to(torch.bfloat16)
+    vt16 = fa.transpose_bf16(v.to(torch.bfloat16))
+    out16 = torch.empty_like(out)
+
+    def fp4_step():
+        fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out)
+
+    def bf16_step():
+        fa.forward_bf16(q16, k16, vt16, softmax_scale=w.softmax_scale, out=out16)
+
+    def quant_step():
+        fa.quantize_qkv(q, k, v)
+
+    # warmup
+    for _ in range(args.warmup):
+        fp4_step()
+        if not args.no_bf16:
+            bf16_step()
+    torch.cuda.synchronize()
+
+    # the timed region: exactly `steps` forward steps, synchronized on both sides
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(args.steps):
+        fp4_step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_start) * 1e3
+    fp4_ms = ev0.elapsed_time(ev1) / args.steps
+
+    fns = {"fp4": fp4_step}
+    if not args.no_bf16:
+        fns["bf16"] = bf16_step
+    med, _ = _time_windows(torch, fns, max(1, args.steps // 2), args.windows)
+    qms, _ = _time_windows(torch, {"quant": quant_step}, 3, 3)
+
+    flops = w.flops
+    tflops = flops / (fp4_ms * 1e-3) / 1e12
+    bf16_tflops = flops / (med["bf16"] * 1e-3) / 1e12 if "bf16" in med else None
+    traffic = _traffic()
+    roof = {
+        "bound": "mfma",
+        "achieved": round(tflops, 2),
+        "peak": MXFP4_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(tflops / MXFP4_PEAK_TFLOPS, 4),
+        "traffic": traffic,
+        "kernel": "fwd_mxfp4_kernel<128, 8, false, false>",
+        "algorithmic_flops_per_launch": flops,
+    }
+    line = {
+        "metric": "MXFP4 attn fwd TFLOPS (4BHN^2d/t), % MXFP4 MFMA peak, speedup vs BF16",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(fp4_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "mxfp4",
+        "data": "synthetic",
+        "config": {"workload": name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "inputs": f"{w.dist} {w.dtype}",
+                   "seed": w.seed, "softmax_scale": w.softmax_scale, "affine": [1.5, 1.2],
+                   "output": "fp32", "parallelism": "single GPU"},
+        "pct_mxfp4_peak": round(100 * tflops / MXFP4_PEAK_TFLOPS, 2),
+        "bf16_tflops": None if bf16_tflops is None else round(bf16_tflops, 2),
+        "bf16_pct_peak": None if bf16_tflops is None else round(100 * bf16_tflops / BF16_PEAK_TFLOPS, 2),
+        "speedup_vs_bf16": None if "bf16" not in med else round(med["bf16"] / med["fp4"], 3),
+        "fp4_ms_median_interleaved": round(med["fp4"], 5),
+        "bf16_ms_median_interleaved": None if "bf16" not in med else round(med["bf16"], 5),
+        "quantize_qkv_ms": round(qms["quant"], 5),
+        "wall_ms_timed_region": round(wall_ms, 3),
+        "roofline": roof,
+        "gpu": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_oracle_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

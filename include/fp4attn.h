@@ -1,0 +1,173 @@
+/*
+ * fp4attn: noncausal full-MXFP4 attention forward with Direct-P probabilities
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Hardware-Aware FP4 FlashAttention-4" (arXiv 2609.04105).  The
+ * forward computes S = Q K^T / sqrt(d), P = softmax(S), O = P V
+ * (eq. attention-intro) with Q, K, P and V all in MXFP4: E2M1 codes plus one
+ * E8M0 amplitude per 32 values (Sec. "Problem 2", Table fp4-formats,
+ * eq. mx-scale).  P is produced by Direct-P (Sec. "Direct-P", Alg. 2): scores
+ * map straight to E2M1 codes through an affine classifier (eq. affine-code-map)
+ * and the row normaliser is the sum of the same rounded codes that the PV
+ * product consumes (Fix 2, eqs. represented-contributions/-output).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensor pointers are DEVICE pointers owned by the caller; the library never
+ *   allocates, frees or keeps them.  Every pointer must be 16-byte aligned.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Arguments are validated synchronously on the host; on success the work is
+ *   enqueued asynchronously on `stream` and the call returns without waiting.
+ *   On any error nothing is enqueued and the outputs are untouched.
+ * - Outputs are fully overwritten; inputs are never written.
+ * - The library holds no global state besides a thread-local error string and
+ *   is safe to call from several host threads.
+ * - MXFP4 layout: E2M1 code = sign << 3 | k, k indexing {0, .5, 1, 1.5, 2, 3,
+ *   4, 6}; two codes per byte, element 2j in bits 3:0 and element 2j+1 in bits
+ *   7:4.  E8M0 byte u: amplitude 2^(u-127), u = 255 is NaN.  A value is
+ *   represented as 2^(u-127) * e2m1(code) / 6: the byte stores the block
+ *   amplitude, not the step (eq. mx-scale).
+ */
+#ifndef FP4ATTN_H
+#define FP4ATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FP4ATTN_OK = 0,
+  FP4ATTN_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad size, enum or scalar */
+  FP4ATTN_ERR_UNSUPPORTED = 2, /* valid but not implemented (head dim not 64 or 128) */
+  FP4ATTN_ERR_HIP = 3          /* the HIP runtime refused the launch; see fp4attn_last_error() */
+} fp4attn_status;
+
+typedef enum {
+  FP4ATTN_F32 = 0,
+  FP4ATTN_BF16 = 1
+} fp4attn_dtype;
+
+/*
+ * MXFP4 quantizer (eq. mx-scale).  Quantizes `batch` row-major [rows, cols]
+ * matrices of `src_dtype` in blocks of 32 consecutive values along `axis`.
+ *
+ *   axis = 1 (Q, K: [N, d]):  codes [batch, rows, cols/2], scales [batch, rows, cols/32].
+ *   axis = 0 (V: [N, d], blocks along the sequence): stored TRANSPOSED,
+ *            codes [batch, cols, rows/2], scales [batch, cols, rows/32].
+ *
+ * Per block with absolute maximum a > 0 the amplitude is 2^floor(log2 a) or
+ * 2^ceil(log2 a) (the two candidates of eq. mx-scale), whichever gives the
+ * smaller squared reconstruction error over the block (ties: the ceiling),
+ * compared exactly.  Exponents clamp to [-127, 127].  An all-zero block gets
+ * u = 0; a block holding NaN or +-Inf gets u = 255 and zero codes.  The sign bit
+ * of each code is the sign bit of its input (so -0.0 encodes as 0x8).
+ *
+ * Errors: INVALID_ARG if a pointer is null or misaligned, batch < 1, rows < 1,
+ * cols < 1, the blocked extent (cols for axis 1, rows for axis 0) is not a
+ * multiple of 32, the other extent is odd for axis 0 (codes pack two per byte),
+ * axis is not 0 or 1, or src_dtype is not a fp4attn_dtype.
+ * The quantizer is not part of the timed forward (the paper times the kernel
+ * on prequantized operands).
+ */
+fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows,
+                                      int64_t cols, int axis, uint8_t* codes, uint8_t* scales,
+                                      void* stream);
+
+/*
+ * Direct-P full-MXFP4 attention forward, noncausal (Sec. "Direct-P", Alg. 2,
+ * eqs. affine-code-map, represented-contributions, represented-output).
+ *
+ *   q_codes  [B, H, N, d/2]  q_scales  [B, H, N, d/32]   (fp4attn_quantize_mxfp4, axis 1)
+ *   k_codes  [B, H, N, d/2]  k_scales  [B, H, N, d/32]   (axis 1)
+ *   vt_codes [B, H, d, N/2]  vt_scales [B, H, d, N/32]   (V quantized with axis 0)
+ *   out      [B, H, N, d] of out_dtype (FP4ATTN_F32 or FP4ATTN_BF16)
+ *
+ * For query row i and 32-key block B the kernel forms the score
+ * y = raw * softmax_scale * log2(e) / 36 (raw = the block-scaled FP4 product,
+ * 36 Qhat.Khat), the block exponent E_B = floor(max_B y), and the codes
+ * q = E2M1(max(0, A (y - E_B + log2 6) + B)) with A = affine_a, B = affine_b
+ * (the paper's `fast` fit is 1.5 / 1.2), evaluated as one fp32 fused
+ * multiply-add per score.  P enters the PV product as MXFP4 with E8M0 byte
+ * E_B - M_i + 127 against an integer running row reference M_i (clamped to
+ * [0, 254]; 0 marks a block more than 127 binades below the reference), and
+ * O_i = sum_B 2^(E_B - M_i) sum_j q_ij Vhat_j / sum_B 2^(E_B - M_i) c_B with
+ * c_B = sum_j q_ij taken from the same codes.
+ *
+ * Errors: INVALID_ARG for null/misaligned pointers, B < 1, H < 1, N < 128 or
+ * N % 128 != 0, softmax_scale not finite or <= 0, affine_a not finite or <= 0,
+ * affine_b not finite, bad out_dtype, or B*H*N beyond 2^31.  UNSUPPORTED for
+ * d not in {64, 128}.  NaN inputs propagate to the affected rows.
+ */
+fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales,
+                                     const uint8_t* k_codes, const uint8_t* k_scales,
+                                     const uint8_t* vt_codes, const uint8_t* vt_scales,
+                                     int64_t B, int64_t H, int64_t N, int64_t d,
+                                     float softmax_scale, float affine_a, float affine_b,
+                                     void* out, int out_dtype, void* stream);
+
+/*
+ * Same-design BF16 attention forward: the speed baseline of the paper's
+ * canonical speedup t_BF16 / t_k (eq. canonical-speedup).  Textbook softmax
+ * attention (eq. exact-attention) with the online recurrence
+ * (eq. online-recurrence) in base 2, fp32 accumulation and P rounded to bf16
+ * for the PV product.
+ *
+ *   q, k [B, H, N, d] bf16;  vt [B, H, d, N] bf16 (V transposed, see
+ *   fp4attn_transpose_bf16);  out [B, H, N, d] of out_dtype.
+ *
+ * Errors: as fp4attn_forward_mxfp4 (no affine arguments).
+ */
+fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* vt,
+                                    int64_t B, int64_t H, int64_t N, int64_t d,
+                                    float softmax_scale, void* out, int out_dtype, void* stream);
+
+/*
+ * Layout helper for the BF16 baseline: dst[b, c, r] = src[b, r, c] for
+ * `batch` bf16 [rows, cols] matrices.  Not part of the timed forward, like the
+ * quantizer.  Errors: INVALID_ARG for null/misaligned pointers, batch/rows/cols
+ * < 1, rows or cols not a multiple of 8.
+ */
+fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols,
+                                      void* dst, void* stream);
+
+/*
+ * Test hook: runs exactly the forward kernel of fp4attn_forward_mxfp4 (same
+ * launch configuration and arguments, writes `out` too) and additionally
+ * dumps the Direct-P state of selected query rows (Alg. 2, steps 1-6):
+ *
+ *   row_ids    [n_rows] int64, flattened (b*H + h)*N + i, STRICTLY ASCENDING
+ *              (rows not found by the kernel's binary search are not dumped)
+ *   p_codes    [n_rows, N/2]  the P codes fed to the PV product, nibble-packed
+ *   block_exp  [n_rows, N/32] int16 absolute block exponents E_B
+ *   row_m      [n_rows] int32 final integer row reference M_i
+ *   row_d      [n_rows] fp32 represented denominator relative to 2^M_i
+ *
+ * Errors: as fp4attn_forward_mxfp4, plus INVALID_ARG for n_rows < 1 or a null
+ * dump pointer.
+ */
+fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales,
+                                           const uint8_t* k_codes, const uint8_t* k_scales,
+                                           const uint8_t* vt_codes, const uint8_t* vt_scales,
+                                           int64_t B, int64_t H, int64_t N, int64_t d,
+                                           float softmax_scale, float affine_a, float affine_b,
+                                           void* out, int out_dtype,
+                                           const int64_t* row_ids, int64_t n_rows,
+                                           uint8_t* p_codes, int16_t* block_exp,
+                                           int32_t* row_m, float* row_d, void* stream);
+
+/* Static description of a status code; never NULL. */
+const char* fp4attn_status_string(int status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* fp4attn_last_error(void);
+
+/* ABI version of this header, (major << 16) | minor. */
+int fp4attn_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FP4ATTN_H */

@@ -26,19 +26,16 @@ def round_index(r):
     r = np.asarray(r, dtype=np.float64)
     if np.any(~np.isfinite(r)) or np.any(r < 0):
         raise ValueError("round_index expects finite, non-negative magnitudes")
-    # Saturate first: for very large r all eight fp64 distances would round equal.
-    # For r <= 6 each distance to a neighbour is exact (Sterbenz: the neighbours
-    # of any r >= 1/2 are within a factor of two of it), so ties are true ties.
     r = np.minimum(r, MAX_MAGNITUDE)
-    dist = np.abs(r[..., None] - MAGNITUDES)
-    best = dist.min(axis=-1, keepdims=True)
-    is_best = dist == best
-    # At a tie exactly two neighbours are minimal, one with even index.
-    even = (np.arange(8) % 2) == 0
-    choice_even = np.argmax(is_best & even, axis=-1)
-    has_even = np.any(is_best & even, axis=-1)
-    choice_any = np.argmax(is_best, axis=-1)
-    return np.where(has_even, choice_even, choice_any).astype(np.uint8)
+    # The nearest entry is one of the two table entries that bracket r.
+    hi = np.clip(np.searchsorted(MAGNITUDES, r, side="right"), 1, 7)
+    lo = hi - 1
+    # Both distances are exact in fp64 (Sterbenz: for r >= 1/2 the bracketing
+    # entries lie within a factor of two of r), so equal distances are true ties.
+    d_lo = r - MAGNITUDES[lo]
+    d_hi = MAGNITUDES[hi] - r
+    take_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (hi % 2 == 0))
+    return np.where(take_hi, hi, lo).astype(np.uint8)
 
 
 def round_value(r):

@@ -1,0 +1,63 @@
+"""ctypes loader for libfp4attn.so and the signatures of its C-ABI entry points."""
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfp4attn.so")
+
+FP4ATTN_OK = 0
+FP4ATTN_F32 = 0
+FP4ATTN_BF16 = 1
+
+_c_p = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_int = ctypes.c_int
+_f32 = ctypes.c_float
+
+# name -> (argtypes); every entry point except the last three returns a status int
+SIGNATURES = {
+    "fp4attn_quantize_mxfp4": [_c_p, _int, _i64, _i64, _i64, _int, _c_p, _c_p, _c_p],
+    "fp4attn_forward_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32] * 3 + [_c_p, _int, _c_p],
+    "fp4attn_forward_bf16": [_c_p] * 3 + [_i64] * 4 + [_f32, _c_p, _int, _c_p],
+    "fp4attn_transpose_bf16": [_c_p, _i64, _i64, _i64, _c_p, _c_p],
+    "fp4attn_debug_directp_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32] * 3 + [_c_p, _int, _c_p, _i64]
+    + [_c_p] * 4 + [_c_p],
+    "fp4attn_status_string": [_int],
+    "fp4attn_last_error": [],
+    "fp4attn_abi_version": [],
+}
+RESTYPES = {"fp4attn_status_string": ctypes.c_char_p, "fp4attn_last_error": ctypes.c_char_p,
+            "fp4attn_abi_version": ctypes.c_int}
+
+
+class Fp4AttnError(RuntimeError):
+    def __init__(self, status, detail):
+        self.status = status
+        super().__init__(f"fp4attn status {status}: {detail}")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2609_04105_amd.build` "
+            "(or __graft_entry__.build()); there is no fallback path")
+    handle = ctypes.CDLL(LIB_PATH)
+    for name, args in SIGNATURES.items():
+        fn = getattr(handle, name)
+        fn.argtypes = args
+        fn.restype = RESTYPES.get(name, ctypes.c_int)
+    return handle
+
+
+lib = _load()
+
+
+def check(status):
+    """Raise Fp4AttnError unless ``status`` is FP4ATTN_OK."""
+    if status != FP4ATTN_OK:
+        detail = lib.fp4attn_last_error().decode() or lib.fp4attn_status_string(status).decode()
+        raise Fp4AttnError(status, detail)
+
+
+def abi_version():
+    v = lib.fp4attn_abi_version()
+    return v >> 16, v & 0xFFFF

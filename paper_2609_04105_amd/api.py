@@ -1,0 +1,158 @@
+"""Torch-facing wrappers of the C-ABI (argument marshalling only).
+
+Shapes follow include/fp4attn.h.  Inputs must be contiguous CUDA (HIP) tensors;
+outputs are allocated with torch unless passed in.  Work is enqueued on the
+current torch stream of the tensors' device.
+"""
+import ctypes
+import math
+
+import torch
+
+from ._lib import FP4ATTN_BF16, FP4ATTN_F32, check, lib
+
+_DTYPES = {torch.float32: FP4ATTN_F32, torch.bfloat16: FP4ATTN_BF16}
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _need(t, name, dtype=None, ndim=None):
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got shape {tuple(t.shape)}")
+
+
+def quantize_mxfp4(x, axis=-1):
+    """MXFP4 codes and E8M0 scales of ``x`` [..., rows, cols] (fp32 or bf16).
+
+    axis=-1: blocks of 32 along cols -> codes [..., rows, cols/2], scales [..., rows, cols/32].
+    axis=-2: blocks along rows, stored transposed -> codes [..., cols, rows/2], scales [..., cols, rows/32].
+    """
+    _need(x, "x", (torch.float32, torch.bfloat16))
+    if x.dim() < 2:
+        raise ValueError("x needs at least two dimensions")
+    lead = tuple(x.shape[:-2])
+    rows, cols = x.shape[-2:]
+    batch = math.prod(lead) if lead else 1
+    if axis in (-1, x.dim() - 1):
+        c_axis, cshape, sshape = 1, lead + (rows, cols // 2), lead + (rows, cols // 32)
+    elif axis in (-2, x.dim() - 2):
+        c_axis, cshape, sshape = 0, lead + (cols, rows // 2), lead + (cols, rows // 32)
+    else:
+        raise ValueError("axis must be -1 or -2")
+    codes = torch.empty(cshape, dtype=torch.uint8, device=x.device)
+    scales = torch.empty(sshape, dtype=torch.uint8, device=x.device)
+    check(lib.fp4attn_quantize_mxfp4(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, _ptr(codes),
+                                     _ptr(scales), _stream(x)))
+    return codes, scales
+
+
+def quantize_qkv(q, k, v):
+    """MXFP4 operands of the forward: Q, K along d; V along the sequence (transposed)."""
+    qc, qs = quantize_mxfp4(q, axis=-1)
+    kc, ks = quantize_mxfp4(k, axis=-1)
+    vc, vs = quantize_mxfp4(v, axis=-2)
+    return qc, qs, kc, ks, vc, vs
+
+
+def _fp4_shape(q_codes):
+    _need(q_codes, "q_codes", torch.uint8, 4)
+    B, H, N, half_d = q_codes.shape
+    return B, H, N, 2 * half_d
+
+
+def _check_operands(B, H, N, d, ops):
+    names = ("q_codes", "q_scales", "k_codes", "k_scales", "vt_codes", "vt_scales")
+    shapes = ((B, H, N, d // 2), (B, H, N, d // 32), (B, H, N, d // 2), (B, H, N, d // 32),
+              (B, H, d, N // 2), (B, H, d, N // 32))
+    for t, name, shape in zip(ops, names, shapes):
+        _need(t, name, torch.uint8, 4)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {shape}")
+
+
+def _out(out, B, H, N, d, out_dtype, device):
+    if out is None:
+        return torch.empty((B, H, N, d), dtype=out_dtype, device=device)
+    _need(out, "out", (torch.float32, torch.bfloat16), 4)
+    if tuple(out.shape) != (B, H, N, d):
+        raise ValueError(f"out has shape {tuple(out.shape)}, expected {(B, H, N, d)}")
+    return out
+
+
+def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, softmax_scale=None,
+                  affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32):
+    """Direct-P full-MXFP4 attention forward; returns O [B, H, N, d]."""
+    B, H, N, d = _fp4_shape(q_codes)
+    ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
+    _check_operands(B, H, N, d, ops)
+    out = _out(out, B, H, N, d, out_dtype, q_codes.device)
+    s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
+    check(lib.fp4attn_forward_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
+                                    _DTYPES[out.dtype], _stream(out)))
+    return out
+
+
+def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, row_ids, softmax_scale=None,
+                        affine_a=1.5, affine_b=1.2, out_dtype=torch.float32):
+    """Forward plus the Direct-P state of the (strictly ascending) flattened ``row_ids``.
+
+    Returns a dict: out, p_codes [R, N/2] uint8, block_exp [R, N/32] int16,
+    row_m [R] int32, row_d [R] fp32.
+    """
+    B, H, N, d = _fp4_shape(q_codes)
+    ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
+    _check_operands(B, H, N, d, ops)
+    _need(row_ids, "row_ids", torch.int64, 1)
+    R = row_ids.numel()
+    dev = q_codes.device
+    out = torch.empty((B, H, N, d), dtype=out_dtype, device=dev)
+    res = {
+        "out": out,
+        "p_codes": torch.empty((R, N // 2), dtype=torch.uint8, device=dev),
+        "block_exp": torch.empty((R, N // 32), dtype=torch.int16, device=dev),
+        "row_m": torch.empty((R,), dtype=torch.int32, device=dev),
+        "row_d": torch.empty((R,), dtype=torch.float32, device=dev),
+    }
+    s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
+    check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
+                                          _DTYPES[out_dtype], _ptr(row_ids), R, _ptr(res["p_codes"]),
+                                          _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),
+                                          _stream(out)))
+    return res
+
+
+def transpose_bf16(v):
+    """V [..., N, d] bf16 -> V^T [..., d, N] (layout preparation of the BF16 baseline)."""
+    _need(v, "v", torch.bfloat16)
+    lead = tuple(v.shape[:-2])
+    rows, cols = v.shape[-2:]
+    vt = torch.empty(lead + (cols, rows), dtype=torch.bfloat16, device=v.device)
+    check(lib.fp4attn_transpose_bf16(_ptr(v), math.prod(lead) if lead else 1, rows, cols, _ptr(vt), _stream(v)))
+    return vt
+
+
+def forward_bf16(q, k, vt, softmax_scale=None, out=None, out_dtype=torch.float32):
+    """Same-design BF16 attention forward; q, k [B, H, N, d], vt [B, H, d, N] bf16."""
+    _need(q, "q", torch.bfloat16, 4)
+    _need(k, "k", torch.bfloat16, 4)
+    _need(vt, "vt", torch.bfloat16, 4)
+    B, H, N, d = q.shape
+    if tuple(k.shape) != (B, H, N, d) or tuple(vt.shape) != (B, H, d, N):
+        raise ValueError("k must be [B, H, N, d] and vt [B, H, d, N]")
+    out = _out(out, B, H, N, d, out_dtype, q.device)
+    s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
+    check(lib.fp4attn_forward_bf16(_ptr(q), _ptr(k), _ptr(vt), B, H, N, d, s, _ptr(out), _DTYPES[out.dtype],
+                                   _stream(out)))
+    return out

@@ -1,0 +1,207 @@
+// C-ABI of libfp4attn: argument validation, status codes, and launch.
+// Declarations and the contract of every entry point are in include/fp4attn.h.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/fp4attn.h"
+#include "launch.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+fp4attn_status fail(fp4attn_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+fp4attn_status fail(fp4attn_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+fp4attn_status ok() {
+  g_last_error[0] = '\0';
+  return FP4ATTN_OK;
+}
+
+fp4attn_status from_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(FP4ATTN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define REQUIRE_PTR(p)                                                                        \
+  do {                                                                                        \
+    if (!aligned16(p)) return fail(FP4ATTN_ERR_INVALID_ARG, "%s is null or not 16-byte aligned", #p); \
+  } while (0)
+
+// Shared checks of the two attention forwards.
+fp4attn_status check_attention_shape(int64_t B, int64_t H, int64_t N, int64_t d, float softmax_scale, int out_dtype) {
+  if (B < 1 || H < 1) return fail(FP4ATTN_ERR_INVALID_ARG, "B=%lld and H=%lld must be >= 1", (long long)B, (long long)H);
+  if (N < 128 || N % 128 != 0)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "N=%lld must be a positive multiple of 128", (long long)N);
+  if (!std::isfinite(softmax_scale) || softmax_scale <= 0.0f)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "softmax_scale must be finite and positive");
+  if (out_dtype != FP4ATTN_F32 && out_dtype != FP4ATTN_BF16)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "out_dtype %d is not FP4ATTN_F32 or FP4ATTN_BF16", out_dtype);
+  if (B * H * N > (int64_t(1) << 31) - 1 || B * H > 65535 * 256)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "B*H*N=%lld exceeds 2^31", (long long)(B * H * N));
+  if (d != 64 && d != 128) return fail(FP4ATTN_ERR_UNSUPPORTED, "head dimension d=%lld is not 64 or 128", (long long)d);
+  return FP4ATTN_OK;
+}
+
+fp4attn_status check_directp(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                             const uint8_t* k_scales, const uint8_t* vt_codes, const uint8_t* vt_scales, int64_t B,
+                             int64_t H, int64_t N, int64_t d, float softmax_scale, float affine_a, float affine_b,
+                             void* out, int out_dtype) {
+  REQUIRE_PTR(q_codes);
+  REQUIRE_PTR(q_scales);
+  REQUIRE_PTR(k_codes);
+  REQUIRE_PTR(k_scales);
+  REQUIRE_PTR(vt_codes);
+  REQUIRE_PTR(vt_scales);
+  REQUIRE_PTR(out);
+  if (!std::isfinite(affine_a) || affine_a <= 0.0f)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "affine_a must be finite and positive");
+  if (!std::isfinite(affine_b)) return fail(FP4ATTN_ERR_INVALID_ARG, "affine_b must be finite");
+  return check_attention_shape(B, H, N, d, softmax_scale, out_dtype);
+}
+
+fp4attn::DirectPArgs directp_args(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                                  const uint8_t* k_scales, const uint8_t* vt_codes, const uint8_t* vt_scales,
+                                  int64_t B, int64_t H, int64_t N, int64_t d, float softmax_scale, float affine_a,
+                                  float affine_b, void* out, int out_dtype) {
+  fp4attn::DirectPArgs a{};
+  a.q_codes = q_codes;
+  a.q_scales = q_scales;
+  a.k_codes = k_codes;
+  a.k_scales = k_scales;
+  a.vt_codes = vt_codes;
+  a.vt_scales = vt_scales;
+  a.out = out;
+  a.B = (int)B;
+  a.H = (int)H;
+  a.N = (int)N;
+  a.d = (int)d;
+  a.out_bf16 = out_dtype == FP4ATTN_BF16;
+  a.softmax_scale = softmax_scale;
+  a.affine_a = affine_a;
+  a.affine_b = affine_b;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols,
+                                      int axis, uint8_t* codes, uint8_t* scales, void* stream) {
+  REQUIRE_PTR(src);
+  REQUIRE_PTR(codes);
+  REQUIRE_PTR(scales);
+  if (src_dtype != FP4ATTN_F32 && src_dtype != FP4ATTN_BF16)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "src_dtype %d is not FP4ATTN_F32 or FP4ATTN_BF16", src_dtype);
+  if (axis != 0 && axis != 1) return fail(FP4ATTN_ERR_INVALID_ARG, "axis %d must be 0 or 1", axis);
+  if (batch < 1 || rows < 1 || cols < 1) return fail(FP4ATTN_ERR_INVALID_ARG, "batch, rows and cols must be >= 1");
+  const int64_t blocked = axis == 1 ? cols : rows, other = axis == 1 ? rows : cols;
+  if (blocked % 32 != 0)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "the blocked extent (%lld) must be a multiple of 32", (long long)blocked);
+  if (batch * other * (blocked / 32) > (int64_t(1) << 40))
+    return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large");
+  if ((batch * other * (blocked / 32) + 255) / 256 > 0x7fffffff)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large for one launch");
+  return from_hip(fp4attn::launch_quantize_mxfp4(src, src_dtype, batch, rows, cols, axis, codes, scales,
+                                                 static_cast<hipStream_t>(stream)),
+                  "quantize launch");
+}
+
+fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                                     const uint8_t* k_scales, const uint8_t* vt_codes, const uint8_t* vt_scales,
+                                     int64_t B, int64_t H, int64_t N, int64_t d, float softmax_scale, float affine_a,
+                                     float affine_b, void* out, int out_dtype, void* stream) {
+  const fp4attn_status st = check_directp(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
+                                          softmax_scale, affine_a, affine_b, out, out_dtype);
+  if (st != FP4ATTN_OK) return st;
+  const fp4attn::DirectPArgs a = directp_args(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
+                                              softmax_scale, affine_a, affine_b, out, out_dtype);
+  return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "forward launch");
+}
+
+fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                                           const uint8_t* k_scales, const uint8_t* vt_codes,
+                                           const uint8_t* vt_scales, int64_t B, int64_t H, int64_t N, int64_t d,
+                                           float softmax_scale, float affine_a, float affine_b, void* out,
+                                           int out_dtype, const int64_t* row_ids, int64_t n_rows, uint8_t* p_codes,
+                                           int16_t* block_exp, int32_t* row_m, float* row_d, void* stream) {
+  const fp4attn_status st = check_directp(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
+                                          softmax_scale, affine_a, affine_b, out, out_dtype);
+  if (st != FP4ATTN_OK) return st;
+  REQUIRE_PTR(row_ids);
+  REQUIRE_PTR(p_codes);
+  REQUIRE_PTR(block_exp);
+  REQUIRE_PTR(row_m);
+  REQUIRE_PTR(row_d);
+  if (n_rows < 1 || n_rows > 0x7fffffff) return fail(FP4ATTN_ERR_INVALID_ARG, "n_rows must be in [1, 2^31)");
+  fp4attn::DirectPArgs a = directp_args(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
+                                        softmax_scale, affine_a, affine_b, out, out_dtype);
+  a.row_ids = row_ids;
+  a.n_rows = (int)n_rows;
+  a.p_codes = p_codes;
+  a.block_exp = block_exp;
+  a.row_m = row_m;
+  a.row_d = row_d;
+  return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "debug forward launch");
+}
+
+fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* vt, int64_t B, int64_t H, int64_t N,
+                                    int64_t d, float softmax_scale, void* out, int out_dtype, void* stream) {
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(k);
+  REQUIRE_PTR(vt);
+  REQUIRE_PTR(out);
+  const fp4attn_status st = check_attention_shape(B, H, N, d, softmax_scale, out_dtype);
+  if (st != FP4ATTN_OK) return st;
+  fp4attn::Bf16Args a{};
+  a.q = q;
+  a.k = k;
+  a.vt = vt;
+  a.out = out;
+  a.B = (int)B;
+  a.H = (int)H;
+  a.N = (int)N;
+  a.d = (int)d;
+  a.out_bf16 = out_dtype == FP4ATTN_BF16;
+  a.softmax_scale = softmax_scale;
+  return from_hip(fp4attn::launch_forward_bf16(a, static_cast<hipStream_t>(stream)), "bf16 forward launch");
+}
+
+fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols, void* dst,
+                                      void* stream) {
+  REQUIRE_PTR(src);
+  REQUIRE_PTR(dst);
+  if (batch < 1 || rows < 1 || cols < 1 || rows % 8 || cols % 8)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "batch, rows, cols must be >= 1 and rows, cols multiples of 8");
+  if (batch > 65535 || (rows + 63) / 64 > 65535)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "batch or rows too large for one launch");
+  return from_hip(fp4attn::launch_transpose_bf16(src, batch, rows, cols, dst, static_cast<hipStream_t>(stream)),
+                  "transpose launch");
+}
+
+const char* fp4attn_status_string(int status) {
+  switch (status) {
+    case FP4ATTN_OK: return "ok";
+    case FP4ATTN_ERR_INVALID_ARG: return "invalid argument";
+    case FP4ATTN_ERR_UNSUPPORTED: return "unsupported configuration";
+    case FP4ATTN_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* fp4attn_last_error(void) { return g_last_error; }
+
+int fp4attn_abi_version(void) { return (1 << 16) | 0; }
+
+}  // extern "C"

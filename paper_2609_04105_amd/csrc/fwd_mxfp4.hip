@@ -1,0 +1,395 @@
+// Direct-P full-MXFP4 attention forward for gfx950.
+//
+// Method (paper Sec. "Direct-P", Alg. 2, eqs. affine-code-map,
+// represented-contributions, represented-output):
+//   raw   = block-scaled FP4 product of Q and K          (= 36 Qhat Khat^T)
+//   E_B   = floor(max_{j in B} raw_ij * c_y)              c_y = s log2(e) / 36
+//   q_ij  = E2M1(max(0, fma(c_a, raw_ij, k0 - A E_B)))     c_a = A c_y, k0 = A log2 6 + B
+//   O_i   = sum_B 2^(E_B - M_i) sum_j q_ij (6 Vhat_j) / (6 sum_B 2^(E_B - M_i) c_B)
+//
+// gfx950 design
+// - One workgroup = NW waves = 32 * NW query rows of one (batch, head); each
+//   wave owns 32 queries for the whole key loop.  Both products run on the
+//   scaled FP4 matrix unit (v_mfma_scale_f32_32x32x64_f8f6f4) in transposed
+//   form: S^T = K Q^T and O^T = V^T P^T.  Lane l then holds query l % 32 in
+//   every accumulator, so the per-row online state (integer reference M_i, the
+//   lazy power-of-two rescale) is a per-lane scalar and needs no cross-lane
+//   broadcast.
+// - K rows are fed to the S^T product in the order pi(m) = 16 h + 4 g + i for
+//   operand row m = 8 g + 4 h + i.  With the 32x32 accumulator layout, lane half
+//   h then holds keys 16 h .. 16 h + 15 of each 32-key block in register order,
+//   so the E2M1 codes come out of the converter already in key order and one
+//   v_permlane32_swap per dword turns two adjacent blocks into the K64 P^T
+//   operand of the PV product (the paper's paired N32 -> K64 publication).
+// - Block maxima: 16 values per lane, then one half-wave exchange.
+// - Code map: one v_fma_f32 with the clamp modifier per score on u / 8, then
+//   v_cvt_scalef32_pk_fp4_f32 with scale 1/8 (two scores per instruction);
+//   the clamp to [0, 1] realises max(0, u) and saturation for free, and scaling
+//   by a power of two leaves every rounding decision unchanged.
+// - Denominator c_B: an extra 32x32x64 product of the same P^T operand with a
+//   constant "ones" row, so it uses exactly the codes and E8M0 bytes of PV and
+//   costs no vector-ALU work.
+// - K/V tiles of 128 keys are staged in LDS in matrix-operand order (each
+//   lane's 16-byte fragment contiguous), double-buffered through registers.
+// - Workgroups are remapped so that the query tiles of one head run on one XCD
+//   and share its L2 copy of that head's K/V.
+#include "gfx950.hpp"
+#include "launch.hpp"
+
+namespace fp4attn {
+
+namespace {
+
+constexpr int kBN = 128;   // keys per LDS tile
+constexpr int kTau = 8;    // lazy rescale: the reference may lag the row maximum by up to 8 binades
+constexpr double kLog2E = 1.4426950408889634;
+constexpr double kLog2Of6 = 2.584962500721156;
+
+struct KParams {
+  const uint8_t* qc;
+  const uint8_t* qs;
+  const uint8_t* kc;
+  const uint8_t* ks;
+  const uint8_t* vc;
+  const uint8_t* vs;
+  void* out;
+  int N, n_qtiles, total;
+  float c_y, c_a8, k0_8, a8;
+  const int64_t* row_ids;
+  int n_rows;
+  uint8_t* p_codes;
+  int16_t* block_exp;
+  int32_t* row_m;
+  float* row_d;
+};
+
+template <int D>
+struct Layout {
+  static constexpr int kCodes = (kBN / 32) * (D / 64) * 1024;  // K fragments [sub][chunk][lane][16 B]
+  static constexpr int kScales = (kBN / 32) * 64 * 4;          // [sub][lane] u32
+  static constexpr int vCodes = (kBN / 64) * (D / 32) * 1024;  // V^T fragments [step][chunk][lane][16 B]
+  static constexpr int vScales = (D / 32) * 64 * 4;            // [chunk][lane] u32
+  static constexpr int kOff = 0;
+  static constexpr int ksOff = kOff + kCodes;
+  static constexpr int vOff = ksOff + kScales;
+  static constexpr int vsOff = vOff + vCodes;
+  static constexpr int stage = vsOff + vScales;
+};
+
+// Key of operand row m (0..31) within a 32-key block, and its inverse.
+__device__ __forceinline__ int key_of_row(int m) { return 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3); }
+__device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * (k >> 4) + (k & 3); }
+
+template <int D, int NW>
+struct TileRegs {
+  static constexpr int NT = NW * 64;
+  static constexpr int nK = Layout<D>::kCodes / 16;
+  static constexpr int nV = Layout<D>::vCodes / 16;
+  static constexpr int KPT = (nK + NT - 1) / NT;
+  static constexpr int VPT = (nV + NT - 1) / NT;
+  v4i k[KPT];
+  v4i v[VPT];
+  unsigned ks, vs;
+
+  __device__ __forceinline__ void load(const uint8_t* kc, const uint8_t* ks_, const uint8_t* vc, const uint8_t* vs_,
+                                       int N, int key0, int tid) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int slot = tid + i * NT;
+      if (nK % NT == 0 || slot < nK) {
+        const int m = slot & 63, rest = slot >> 6;
+        const int c = rest % (D / 64), sub = rest / (D / 64);
+        const int key = sub * 32 + key_of_row(m & 31);
+        const int j = 2 * c + (m >> 5);
+        k[i] = *reinterpret_cast<const v4i*>(kc + (size_t)(key0 + key) * (D / 2) + j * 16);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int slot = tid + i * NT;
+      if (nV % NT == 0 || slot < nV) {
+        const int m = slot & 63, rest = slot >> 6;
+        const int cc = rest % (D / 32), s = rest / (D / 32);
+        const int row = cc * 32 + (m & 31);
+        v[i] = *reinterpret_cast<const v4i*>(vc + (size_t)row * (N / 2) + key0 / 2 + s * 32 + (m >> 5) * 16);
+      }
+    }
+    if (tid < kBN) {
+      const uint8_t* p = ks_ + (size_t)(key0 + tid) * (D / 32);
+      ks = D == 128 ? *reinterpret_cast<const uint32_t*>(p) : (unsigned)*reinterpret_cast<const uint16_t*>(p);
+    } else if (tid < kBN + D) {
+      const int row = tid - kBN;
+      vs = *reinterpret_cast<const uint32_t*>(vs_ + (size_t)row * (N / 32) + key0 / 32);
+    }
+  }
+
+  __device__ __forceinline__ void store(uint8_t* st, int tid) const {
+    using L = Layout<D>;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int slot = tid + i * NT;
+      if (nK % NT == 0 || slot < nK) *reinterpret_cast<v4i*>(st + L::kOff + slot * 16) = k[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int slot = tid + i * NT;
+      if (nV % NT == 0 || slot < nV) *reinterpret_cast<v4i*>(st + L::vOff + slot * 16) = v[i];
+    }
+    if (tid < kBN) {
+      const int sub = tid >> 5, m0 = row_of_key(tid & 31);
+      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::ksOff) + sub * 64;
+      dst[m0] = ks;            // lanes 0..31 use scale bytes 0, 2 (d blocks 0, 2)
+      dst[m0 + 32] = ks >> 8;  // lanes 32..63 use bytes 1, 3
+    } else if (tid < kBN + D) {
+      const int row = tid - kBN, cc = row >> 5, m0 = row & 31;
+      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::vsOff) + cc * 64;
+      dst[m0] = vs;
+      dst[m0 + 32] = vs >> 8;
+    }
+  }
+};
+
+template <int D, int NW, bool DUMP, bool OUT_BF16>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_mxfp4_kernel(const KParams p) {
+  using L = Layout<D>;
+  constexpr int BM = NW * 32;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * L::stage];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, lr = lane & 31;
+  const int lin = xcd_remap(blockIdx.x, p.total);
+  const int bh = lin / p.n_qtiles, qt = lin % p.n_qtiles;
+  const int N = p.N;
+  const int qrow = qt * BM + wave * 32 + lr;
+
+  const uint8_t* kc = p.kc + (size_t)bh * N * (D / 2);
+  const uint8_t* ks = p.ks + (size_t)bh * N * (D / 32);
+  const uint8_t* vc = p.vc + (size_t)bh * D * (N / 2);
+  const uint8_t* vs = p.vs + (size_t)bh * D * (N / 32);
+
+  // Q^T operand, resident for the whole key loop.
+  v4i qf[D / 64];
+  {
+    const uint8_t* qrow_codes = p.qc + ((size_t)bh * N + qrow) * (D / 2);
+#pragma unroll
+    for (int c = 0; c < D / 64; ++c) qf[c] = *reinterpret_cast<const v4i*>(qrow_codes + (2 * c + h) * 16);
+  }
+  int qsc;
+  {
+    const uint8_t* qs = p.qs + ((size_t)bh * N + qrow) * (D / 32);
+    const unsigned raw = D == 128 ? *reinterpret_cast<const uint32_t*>(qs) : *reinterpret_cast<const uint16_t*>(qs);
+    qsc = (int)(raw >> (8 * h));
+  }
+
+  int slot = -1;
+  if constexpr (DUMP) {
+    const int64_t g = (int64_t)bh * N + qrow;
+    int lo = 0, hi = p.n_rows - 1;
+    while (lo <= hi) {
+      const int mid = (lo + hi) >> 1;
+      const int64_t v = p.row_ids[mid];
+      if (v == g) {
+        slot = mid;
+        break;
+      }
+      if (v < g) lo = mid + 1;
+      else hi = mid - 1;
+    }
+  }
+
+  const int ones_word = lr == 0 ? 0x22222222 : 0;  // E2M1 1.0 in every nibble of row 0
+  const v4i ones = {ones_word, ones_word, ones_word, ones_word};
+
+  v16f O[D / 32];
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c) O[c] = v16f{};
+  v16f Dacc = v16f{};
+  int Mref = -(1 << 20);  // no block seen yet
+
+  TileRegs<D, NW> regs;
+  regs.load(kc, ks, vc, vs, N, 0, tid);
+  regs.store(lds, tid);
+  __syncthreads();
+
+  const int ntiles = N / kBN;
+  for (int kt = 0; kt < ntiles; ++kt) {
+    uint8_t* st = lds + (kt & 1) * L::stage;
+    if (kt + 1 < ntiles) regs.load(kc, ks, vc, vs, N, (kt + 1) * kBN, tid);
+    const int key0 = kt * kBN;
+
+    static_for<kBN / 64>([&](auto S_) {
+      constexpr int s = decltype(S_)::value;
+      // S^T for the two 32-key blocks of this 64-key step.
+      v16f acc[2];
+      static_for<2>([&](auto T_) {
+        constexpr int sub = 2 * s + decltype(T_)::value;
+        v16f a = v16f{};
+        const int ksc = reinterpret_cast<const int*>(st + L::ksOff)[sub * 64 + lane];
+        static_for<D / 64>([&](auto C_) {
+          constexpr int c = decltype(C_)::value;
+          const v4i kf = *reinterpret_cast<const v4i*>(st + L::kOff + ((sub * (D / 64) + c) * 64 + lane) * 16);
+          a = mfma_fp4_32x32x64<2 * c, 2 * c>(kf, qf[c], a, ksc, qsc);
+        });
+        acc[decltype(T_)::value] = a;
+      });
+
+      // Block maxima (Alg. 2, step 1): 16 scores per lane, then across halves.
+      float m0 = acc[0][0], m1 = acc[1][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) {
+        m0 = fmaxf(m0, acc[0][r]);
+        m1 = fmaxf(m1, acc[1][r]);
+      }
+      unsigned xa = as_uint(m0), xb = as_uint(m1);
+      swap_halves(xa, xb);  // lower: (own m0, partner m0); upper: (partner m1, own m1)
+      const float mx = fmaxf(as_float(xa), as_float(xb));
+      unsigned ya = as_uint(mx), yb = ya;
+      swap_halves(ya, yb);  // every lane: (block-0 max, block-1 max)
+      // Block exponents (step 2).
+      const float E0 = floorf(as_float(ya) * p.c_y);
+      const float E1 = floorf(as_float(yb) * p.c_y);
+      const int E0i = (int)E0, E1i = (int)E1;
+      // Online integer reference with a lazy, exact power-of-two rescale.
+      const int Enew = max(E0i, E1i);
+      const bool need = Enew > Mref + kTau;
+      if (__builtin_amdgcn_ballot_w64(need)) {
+        const int Mn = need ? Enew : Mref;
+        const int sh = Mref - Mn;
+#pragma unroll
+        for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
+        Dacc[0] = ldexpf(Dacc[0], sh);
+        Mref = Mn;
+      }
+      const int u0 = min(max(E0i - Mref + 127, 0), 254);
+      const int u1 = min(max(E1i - Mref + 127, 0), 254);
+      const int ulane = h ? u1 : u0;
+      // Code map (steps 3-4) on u / 8.
+      const float c00 = fmaf(-p.a8, E0, p.k0_8);
+      const float c01 = fmaf(-p.a8, E1, p.k0_8);
+      unsigned X0 = 0, X1 = 0, Y0 = 0, Y1 = 0;
+      static_for<4>([&](auto I_) {
+        constexpr int i = decltype(I_)::value;
+        const float a0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i], c00), 0.0f, 1.0f);
+        const float a1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i + 1], c00), 0.0f, 1.0f);
+        const float a2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i], c00), 0.0f, 1.0f);
+        const float a3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i + 1], c00), 0.0f, 1.0f);
+        const float b0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i], c01), 0.0f, 1.0f);
+        const float b1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i + 1], c01), 0.0f, 1.0f);
+        const float b2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i], c01), 0.0f, 1.0f);
+        const float b3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i + 1], c01), 0.0f, 1.0f);
+        X0 = cvt_pk_fp4<i>(X0, a0, a1, 0.125f);
+        X1 = cvt_pk_fp4<i>(X1, a2, a3, 0.125f);
+        Y0 = cvt_pk_fp4<i>(Y0, b0, b1, 0.125f);
+        Y1 = cvt_pk_fp4<i>(Y1, b2, b3, 0.125f);
+      });
+      // Pair the two blocks into the K64 P^T operand: lower half <- block 0, upper <- block 1.
+      swap_halves(X0, Y0);
+      swap_halves(X1, Y1);
+      const v4i P = {(int)X0, (int)X1, (int)Y0, (int)Y1};
+
+      if constexpr (DUMP) {
+        if (slot >= 0) {
+          const int kb = (key0 + 64 * s) / 32 + h;
+          *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
+          p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)(h ? E1i : E0i);
+        }
+      }
+
+      // PV (step 6 numerator) and the represented denominator from the same operand.
+      static_for<D / 32>([&](auto C_) {
+        constexpr int c = decltype(C_)::value;
+        const v4i vf = *reinterpret_cast<const v4i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 16);
+        const int vsc = reinterpret_cast<const int*>(st + L::vsOff)[c * 64 + lane];
+        O[c] = mfma_fp4_32x32x64<2 * s, 0>(vf, P, O[c], vsc, ulane);
+      });
+      Dacc = mfma_fp4_32x32x64<0, 0>(ones, P, Dacc, 127, ulane);
+    });
+
+    if (kt + 1 < ntiles) regs.store(lds + ((kt + 1) & 1) * L::stage, tid);
+    __syncthreads();
+  }
+
+  // Epilogue: O = acc / (6 D).  The denominator sits in register 0 of the lower half.
+  unsigned d0 = as_uint(Dacc[0]), d1 = d0;
+  swap_halves(d0, d1);
+  const float Dfin = as_float(d0);
+  const float inv = 1.0f / (6.0f * Dfin);
+  const size_t orow = ((size_t)bh * N + qrow) * D;
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int col = 32 * c + 8 * g + 4 * h;
+      const float o0 = O[c][4 * g] * inv, o1 = O[c][4 * g + 1] * inv;
+      const float o2 = O[c][4 * g + 2] * inv, o3 = O[c][4 * g + 3] * inv;
+      if constexpr (OUT_BF16) {
+        typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+        const unsigned w0 = __builtin_bit_cast(unsigned, bf2{(__bf16)o0, (__bf16)o1});
+        const unsigned w1 = __builtin_bit_cast(unsigned, bf2{(__bf16)o2, (__bf16)o3});
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.out) + orow + col) = uint2{w0, w1};
+      } else {
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.out) + orow + col) = float4{o0, o1, o2, o3};
+      }
+    }
+  }
+  if constexpr (DUMP) {
+    if (slot >= 0 && h == 0) {
+      p.row_m[slot] = Mref;
+      p.row_d[slot] = Dfin;
+    }
+  }
+}
+
+template <int D, int NW, bool DUMP, bool OUT_BF16>
+hipError_t launch_variant(const KParams& kp, hipStream_t stream) {
+  hipLaunchKernelGGL((fwd_mxfp4_kernel<D, NW, DUMP, OUT_BF16>), dim3(kp.total), dim3(NW * 64), 0, stream, kp);
+  return hipGetLastError();
+}
+
+template <int D, int NW>
+hipError_t dispatch_flags(const KParams& kp, bool dump, bool out_bf16, hipStream_t stream) {
+  if (dump) return out_bf16 ? launch_variant<D, NW, true, true>(kp, stream) : launch_variant<D, NW, true, false>(kp, stream);
+  return out_bf16 ? launch_variant<D, NW, false, true>(kp, stream) : launch_variant<D, NW, false, false>(kp, stream);
+}
+
+}  // namespace
+
+hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
+  KParams kp{};
+  kp.qc = a.q_codes;
+  kp.qs = a.q_scales;
+  kp.kc = a.k_codes;
+  kp.ks = a.k_scales;
+  kp.vc = a.vt_codes;
+  kp.vs = a.vt_scales;
+  kp.out = a.out;
+  kp.N = a.N;
+  // fp32 coefficients of the folded code map (see the file header).
+  const double s = (double)a.softmax_scale, A = (double)a.affine_a, Bc = (double)a.affine_b;
+  kp.c_y = (float)(s * kLog2E / 36.0);
+  const float c_a = (float)(A * s * kLog2E / 36.0);
+  const float k0 = (float)(A * kLog2Of6 + Bc);
+  kp.c_a8 = c_a * 0.125f;
+  kp.k0_8 = k0 * 0.125f;
+  kp.a8 = a.affine_a * 0.125f;
+  kp.row_ids = a.row_ids;
+  kp.n_rows = a.n_rows;
+  kp.p_codes = a.p_codes;
+  kp.block_exp = a.block_exp;
+  kp.row_m = a.row_m;
+  kp.row_d = a.row_d;
+  const bool dump = a.row_ids != nullptr;
+  const int bh = a.B * a.H;
+  // Eight waves (256 rows) per workgroup when that still fills the 256 CUs.
+  const bool wide = (a.N % 256 == 0) && (int64_t)(a.N / 256) * bh >= 256;
+  const int BM = wide ? 256 : 128;
+  kp.n_qtiles = a.N / BM;
+  kp.total = kp.n_qtiles * bh;
+  if (a.d == 128)
+    return wide ? dispatch_flags<128, 8>(kp, dump, a.out_bf16, stream) : dispatch_flags<128, 4>(kp, dump, a.out_bf16, stream);
+  return wide ? dispatch_flags<64, 8>(kp, dump, a.out_bf16, stream) : dispatch_flags<64, 4>(kp, dump, a.out_bf16, stream);
+}
+
+}  // namespace fp4attn

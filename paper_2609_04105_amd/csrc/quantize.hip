@@ -1,0 +1,161 @@
+// MXFP4 input quantizer and the bf16 transpose used by the BF16 baseline.
+//
+// Quantizer (eq. mx-scale): per block of 32 values with absolute maximum a,
+// the E8M0 amplitude is 2^floor(log2 a) or 2^ceil(log2 a), whichever has the
+// smaller squared reconstruction error (ties keep the ceiling).  With
+// r = 6|v| / 2^e_ceil, ceiling codes qc = E2M1(r) and floor codes qf = E2M1(2r),
+// the floor wins iff sum (2 qc - qf)(4 r - qf - 2 qc) < 0; every term of that
+// sum is exact in fp64 for fp32/bf16 inputs, so the choice is exact.
+// One thread owns one block; the kernel is HBM-bound.
+#include "gfx950.hpp"
+#include "launch.hpp"
+
+namespace fp4attn {
+
+// Index k of the E2M1 magnitude {0, .5, 1, 1.5, 2, 3, 4, 6} nearest to r >= 0,
+// ties to even k, saturating: count the boundaries at or below r, each tie
+// counted toward the even neighbour.
+__device__ __forceinline__ int e2m1_index(double r) {
+  return (r > 0.25) + (r >= 0.75) + (r > 1.25) + (r >= 1.75) + (r > 2.5) + (r >= 3.5) + (r > 5.0);
+}
+__device__ __forceinline__ double e2m1_value(int k) {
+  // 0, .5, 1, 1.5 for k < 4; 2, 3, 4, 6 for k >= 4
+  return k < 4 ? 0.5 * k : (k == 7 ? 6.0 : (double)(k - 2));
+}
+
+template <typename T>
+__device__ __forceinline__ float load_as_float(const T* p);
+template <>
+__device__ __forceinline__ float load_as_float<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float load_as_float<uint16_t>(const uint16_t* p) {
+  return __builtin_bit_cast(float, (unsigned)(*p) << 16);
+}
+
+// axis == 1: blocks along the contiguous axis (Q, K).  axis == 0: blocks along
+// rows, output transposed (V).
+template <typename T, int AXIS>
+__global__ __launch_bounds__(256) void quantize_mxfp4_kernel(const T* __restrict__ src, int64_t batch, int64_t rows,
+                                                             int64_t cols, uint8_t* __restrict__ codes,
+                                                             uint8_t* __restrict__ scales) {
+  const int64_t nblk = AXIS == 1 ? cols / 32 : rows / 32;
+  const int64_t outer = AXIS == 1 ? rows : cols;
+  const int64_t total = batch * outer * nblk;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= total) return;
+  int64_t b, o, blk;
+  if (AXIS == 1) {  // consecutive threads take consecutive blocks of one row
+    blk = t % nblk;
+    o = (t / nblk) % outer;
+    b = t / (nblk * outer);
+  } else {  // consecutive threads take consecutive columns: coalesced loads
+    o = t % outer;
+    blk = (t / outer) % nblk;
+    b = t / (outer * nblk);
+  }
+  float v[32];
+  if (AXIS == 1) {
+    const T* p = src + (b * rows + o) * cols + blk * 32;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + j);
+  } else {
+    const T* p = src + (b * rows + blk * 32) * cols + o;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + (int64_t)j * cols);
+  }
+  float amax = 0.0f;
+  bool finite = true;
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    finite = finite && __builtin_isfinite(v[j]);
+    amax = fmaxf(amax, fabsf(v[j]));
+  }
+  int e = 0;
+  unsigned ubyte;
+  if (!finite) {
+    ubyte = 255;
+  } else if (amax == 0.0f) {
+    ubyte = 0;
+  } else {
+    int x;
+    const float m = frexpf(amax, &x);  // amax = m 2^x, m in [0.5, 1)
+    const int e_floor = x - 1;
+    const int e_ceil = (m == 0.5f) ? x - 1 : x;
+    double delta = 0.0;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const double r = ldexp(6.0 * (double)fabsf(v[j]), -e_ceil);
+      const double qc = e2m1_value(e2m1_index(r));
+      const double qf = e2m1_value(e2m1_index(2.0 * r));
+      delta += (2.0 * qc - qf) * (4.0 * r - qf - 2.0 * qc);
+    }
+    e = (e_floor != e_ceil && delta < 0.0) ? e_floor : e_ceil;
+    e = e < -127 ? -127 : (e > 127 ? 127 : e);
+    ubyte = (unsigned)(e + 127);
+  }
+  unsigned w[4] = {0u, 0u, 0u, 0u};
+  if (finite) {
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const int k = e2m1_index(ldexp(6.0 * (double)fabsf(v[j]), -e));
+      const unsigned code = (unsigned)k | (__builtin_signbit(v[j]) ? 8u : 0u);
+      w[j / 8] |= code << (4 * (j % 8));
+    }
+  }
+  uint8_t* cdst = codes + (b * outer + o) * (nblk * 16) + blk * 16;
+  *reinterpret_cast<v4i*>(cdst) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  scales[(b * outer + o) * nblk + blk] = (uint8_t)ubyte;
+}
+
+// dst[b, c, r] = src[b, r, c] for bf16, through a 64 x 64 LDS tile.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ src, int64_t rows,
+                                                             int64_t cols, uint16_t* __restrict__ dst) {
+  __shared__ uint16_t tile[64][64 + 2];
+  const int64_t b = blockIdx.z;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const uint16_t* s = src + b * rows * cols;
+  uint16_t* d = dst + b * rows * cols;
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int rr = i / 64, cc = i % 64;
+    if (r0 + rr < rows && c0 + cc < cols) tile[rr][cc] = s[(r0 + rr) * cols + c0 + cc];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int cc = i / 64, rr = i % 64;
+    if (r0 + rr < rows && c0 + cc < cols) d[(c0 + cc) * rows + r0 + rr] = tile[rr][cc];
+  }
+}
+
+hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
+                                 uint8_t* codes, uint8_t* scales, hipStream_t stream) {
+  const int64_t nblk = axis == 1 ? cols / 32 : rows / 32;
+  const int64_t outer = axis == 1 ? rows : cols;
+  const int64_t total = batch * outer * nblk;
+  const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  if (src_dtype == 0) {
+    if (axis == 1)
+      hipLaunchKernelGGL((quantize_mxfp4_kernel<float, 1>), grid, block, 0, stream, (const float*)src, batch, rows,
+                         cols, codes, scales);
+    else
+      hipLaunchKernelGGL((quantize_mxfp4_kernel<float, 0>), grid, block, 0, stream, (const float*)src, batch, rows,
+                         cols, codes, scales);
+  } else {
+    if (axis == 1)
+      hipLaunchKernelGGL((quantize_mxfp4_kernel<uint16_t, 1>), grid, block, 0, stream, (const uint16_t*)src, batch,
+                         rows, cols, codes, scales);
+    else
+      hipLaunchKernelGGL((quantize_mxfp4_kernel<uint16_t, 0>), grid, block, 0, stream, (const uint16_t*)src, batch,
+                         rows, cols, codes, scales);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols, void* dst,
+                                 hipStream_t stream) {
+  const dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64), (unsigned)batch), block(256);
+  hipLaunchKernelGGL(transpose_bf16_kernel, grid, block, 0, stream, (const uint16_t*)src, rows, cols,
+                     (uint16_t*)dst);
+  return hipGetLastError();
+}
+
+}  // namespace fp4attn

@@ -1,0 +1,85 @@
+"""Helpers shared by the GPU parity tests: oracle runs on selected rows and the
+comparison metrics.  Imports the oracle (test infrastructure) and, lazily, the
+HIP binding; nothing here is used by the product path."""
+import numpy as np
+import torch
+
+import workloads
+from oracle import directp, e2m1, mxfp4
+
+CODE_MISMATCH_MAX = 1e-4   # fraction of Direct-P codes allowed to differ (rounding ties)
+O_REL_L2_MAX = 2e-3        # output relative L2 error bound
+O_COS_MIN = 0.9999         # output cosine bound
+
+
+def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_codes=True):
+    """Run the oracle on flattened query ``rows`` of fp64 arrays q, k, v [B, H, N, d].
+
+    The oracle quantizes its own operands (oracle.mxfp4).  Returns a dict of
+    row-aligned arrays: O, E, M, D and (optionally) codes.
+    """
+    B, H, N, d = q.shape
+    rows = np.asarray(rows, dtype=np.int64)
+    heads = rows // N
+    out = {"O": np.zeros((len(rows), d)), "E": np.zeros((len(rows), N // 32), dtype=np.int64),
+           "M": np.zeros(len(rows), dtype=np.int64), "D": np.zeros(len(rows))}
+    if want_codes:
+        out["codes"] = np.zeros((len(rows), N), dtype=np.uint8)
+    for bh in np.unique(heads):
+        b, h = divmod(int(bh), H)
+        sel = np.nonzero(heads == bh)[0]
+        local = rows[sel] % N
+        qc, qs = mxfp4.quantize(q[b, h][local], axis=-1)
+        kc, ks = mxfp4.quantize(k[b, h], axis=-1)
+        vc, vs = mxfp4.quantize(v[b, h], axis=-2)
+        res = directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(local)), softmax_scale,
+                                   affine_a, affine_b, want_codes=want_codes)
+        for key in res:
+            out[key][sel] = res[key]
+    return out
+
+
+def rel_l2_cos(a, b):
+    a = np.asarray(a, dtype=np.float64).ravel()
+    b = np.asarray(b, dtype=np.float64).ravel()
+    rel = np.linalg.norm(a - b) / np.linalg.norm(b)
+    cos = a @ b / (np.linalg.norm(a) * np.linalg.norm(b))
+    return float(rel), float(cos)
+
+
+def unpack_codes(packed):
+    """GPU p_codes [R, N/2] -> nibble codes [R, N] (uint8)."""
+    return e2m1.unpack_nibbles(np.asarray(packed, dtype=np.uint8))
+
+
+def gpu_operands(q, k, v):
+    """Quantize torch GPU tensors with the HIP quantizer."""
+    import paper_2609_04105_amd as fa
+    return fa.quantize_qkv(q, k, v)
+
+
+def load_workload(name, device="cuda", **override):
+    """(q, k, v) on the CPU (workload dtype), their fp64 NumPy copies and GPU copies."""
+    q, k, v = workloads.generate(name, **override)
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    dev = tuple(t.to(device) for t in (q, k, v))
+    return host64, dev
+
+
+def check_directp_dump(dump, ref, label):
+    """Assert the Direct-P dump of the GPU against the oracle (codes, E, M, D)."""
+    codes = unpack_codes(dump["p_codes"].cpu().numpy())
+    mag = codes & 7
+    neg = (codes & 8) != 0
+    assert not np.any(neg & (mag != 0)), f"{label}: a nonzero P code carries a sign bit"
+    mismatch = float(np.mean(mag != ref["codes"]))
+    assert mismatch <= CODE_MISMATCH_MAX, f"{label}: code mismatch fraction {mismatch:.3e}"
+    E = dump["block_exp"].cpu().numpy().astype(np.int64)
+    e_mismatch = float(np.mean(E != ref["E"]))
+    assert e_mismatch <= CODE_MISMATCH_MAX, f"{label}: block exponent mismatch fraction {e_mismatch:.3e}"
+    M = dump["row_m"].cpu().numpy().astype(np.int64)
+    assert np.all((M <= ref["M"]) & (M >= ref["M"] - 8)), f"{label}: row reference outside [M - 8, M]"
+    D = dump["row_d"].cpu().numpy().astype(np.float64) * np.exp2(M - ref["M"])
+    rel = np.abs(D - ref["D"]) / ref["D"]
+    assert rel.max() < 1e-4, f"{label}: denominator rel error {rel.max():.3e}"
+    return mismatch

@@ -1,0 +1,81 @@
+"""CPU checks of the C-ABI boundary: the library loads, exports every entry
+point declared in include/fp4attn.h, and rejects bad arguments before any HIP
+call (no compute is launched here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fp4attn.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fp4attn_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2609_04105_amd as fa
+    return fa.lib
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    assert {"fp4attn_quantize_mxfp4", "fp4attn_forward_mxfp4", "fp4attn_forward_bf16"} <= set(names)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    raw = ctypes.CDLL(lib._name)
+    for name in _declared():
+        assert hasattr(raw, name), name
+
+
+def test_binding_covers_every_symbol():
+    from paper_2609_04105_amd import _lib
+    assert set(_declared()) == set(_lib.SIGNATURES)
+
+
+def test_status_strings(lib):
+    assert lib.fp4attn_status_string(0) == b"ok"
+    assert lib.fp4attn_status_string(2) == b"unsupported configuration"
+    assert lib.fp4attn_status_string(99) == b"unknown status"
+    assert lib.fp4attn_abi_version() >> 16 == 1
+
+
+FAKE = [ctypes.c_void_p(4096 * (i + 1)) for i in range(8)]   # aligned, never dereferenced
+
+
+def test_forward_validation(lib):
+    f = lib.fp4attn_forward_mxfp4
+    assert f(None, *FAKE[:5], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1
+    assert b"q_codes" in lib.fp4attn_last_error()
+    assert f(*FAKE[:6], 0, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1
+    assert f(*FAKE[:6], 1, 1, 100, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1
+    assert f(*FAKE[:6], 1, 1, 64, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1
+    assert f(*FAKE[:6], 1, 1, 128, 96, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 2
+    assert f(*FAKE[:6], 1, 1, 128, 64, float("nan"), 1.5, 1.2, FAKE[6], 0, None) == 1
+    assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, -1.0, 1.2, FAKE[6], 0, None) == 1
+    assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, float("inf"), FAKE[6], 0, None) == 1
+    assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 3, None) == 1
+    assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, ctypes.c_void_p(4100), 0, None) == 1
+    assert f(*FAKE[:6], 1 << 20, 1 << 10, 1 << 12, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1
+
+
+def test_quantize_and_bf16_validation(lib):
+    q = lib.fp4attn_quantize_mxfp4
+    assert q(FAKE[0], 0, 1, 4, 48, 1, FAKE[1], FAKE[2], None) == 1     # cols not /32
+    assert q(FAKE[0], 0, 1, 48, 4, 0, FAKE[1], FAKE[2], None) == 1     # rows not /32
+    assert q(FAKE[0], 2, 1, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # dtype
+    assert q(FAKE[0], 0, 1, 4, 64, 2, FAKE[1], FAKE[2], None) == 1     # axis
+    assert q(FAKE[0], 0, 0, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # batch
+    b = lib.fp4attn_forward_bf16
+    assert b(*FAKE[:3], 1, 1, 128, 80, 0.125, FAKE[4], 0, None) == 2
+    assert b(None, *FAKE[1:3], 1, 1, 128, 64, 0.125, FAKE[4], 0, None) == 1
+    t = lib.fp4attn_transpose_bf16
+    assert t(FAKE[0], 1, 7, 8, FAKE[1], None) == 1
+    d = lib.fp4attn_debug_directp_mxfp4
+    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, FAKE[7], 0, *FAKE[:4], None) == 1

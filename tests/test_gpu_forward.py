@@ -1,0 +1,137 @@
+"""GPU parity of the Direct-P MXFP4 forward against the oracle.
+
+Gates (the benchmark spec): Direct-P code mismatch fraction <= 1e-4, output
+relative L2 <= 2e-3 and cosine >= 0.9999; all rows for the small workloads,
+4096 sampled rows (the same launch as the timed forward) for the large ones.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from parity import (O_COS_MIN, O_REL_L2_MAX, check_directp_dump, gpu_operands, load_workload, oracle_rows,
+                    rel_l2_cos)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fa():
+    import paper_2609_04105_amd as fa
+    return fa
+
+
+def _run_and_check(fa, host64, dev, rows, label, softmax_scale=None, affine=(1.5, 1.2)):
+    q, k, v = host64
+    B, H, N, d = q.shape
+    s = 1.0 / np.sqrt(d) if softmax_scale is None else softmax_scale
+    ops = gpu_operands(*dev)
+    row_ids = torch.from_numpy(np.asarray(rows, dtype=np.int64)).cuda()
+    print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)}", flush=True)
+    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, affine_a=affine[0], affine_b=affine[1])
+    out = fa.forward_mxfp4(*ops, softmax_scale=s, affine_a=affine[0], affine_b=affine[1])
+    torch.cuda.synchronize()
+    # the test hook runs the same kernel: identical output
+    assert torch.equal(out, dump["out"]), f"{label}: debug launch output differs from the forward"
+    ref = oracle_rows(q, k, v, rows, s, *affine)
+    mismatch = check_directp_dump(dump, ref, label)
+    got = out.reshape(-1, d)[torch.from_numpy(np.asarray(rows)).cuda()].cpu().numpy()
+    rel, cos = rel_l2_cos(got, ref["O"])
+    print(f"[{label}] code mismatch {mismatch:.2e}  O rel-L2 {rel:.3e}  cos {cos:.8f}", flush=True)
+    assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{label}: rel {rel} cos {cos}"
+    return out, ops
+
+
+def test_tiny_all_rows(fa):
+    host64, dev = load_workload("tiny_b1h1_n128_d64")
+    _run_and_check(fa, host64, dev, workloads.sampled_rows("tiny_b1h1_n128_d64"), "tiny")
+
+
+def test_small_all_rows(fa):
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    _run_and_check(fa, host64, dev, workloads.sampled_rows("small_b1h8_n1024_d64"), "small")
+
+
+@pytest.mark.parametrize("N,d", [(384, 128), (640, 64), (1152, 128)])
+def test_ragged_tiles_all_rows(fa, N, d):
+    """Several key tiles and a query-tile count that does not fill whole 8-wave groups."""
+    g = torch.Generator().manual_seed(N + d)
+    q, k, v = (torch.randn(1, 2, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(2 * N), f"ragged N{N} d{d}")
+
+
+def test_wide_launch_sampled(fa):
+    """The 8-wave (256-row) workgroup path at a size the oracle checks on every 7th row."""
+    g = torch.Generator().manual_seed(7)
+    B, H, N, d = 1, 128, 512, 128
+    q, k, v = (torch.randn(B, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, B * H * N, 7), "wide")
+
+
+@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "student_t_b1h32_n8192_d128",
+                                  "long_b1h32_n16384_d128"])
+def test_full_size_sampled_rows(fa, name):
+    host64, dev = load_workload(name)
+    _run_and_check(fa, host64, dev, workloads.sampled_rows(name), name)
+
+
+def test_affine_variant_and_scale(fa):
+    """The Wan fit (A, B) = (1.6, 0.95) and a non-default softmax scale."""
+    host64, dev = load_workload("small_b1h8_n1024_d64", H=2)
+    _run_and_check(fa, host64, dev, np.arange(2 * 1024), "wan affine", softmax_scale=0.2, affine=(1.6, 0.95))
+
+
+def test_extreme_logits_stay_finite(fa):
+    """Rows whose log2 range exceeds the E8M0 byte range (zero blocks, reference jumps)."""
+    g = torch.Generator().manual_seed(11)
+    N, d = 1024, 128
+    q, k, v = (torch.randn(1, 1, N, d, generator=g) for _ in range(3))
+    q[..., :4] *= 30.0
+    k[..., :4] *= 30.0
+    q, k, v = (t.to(torch.bfloat16) for t in (q, k, v))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    out, _ = _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(N), "extreme")
+    assert torch.isfinite(out).all()
+
+
+def test_deterministic_and_fully_overwritten(fa):
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    ops = gpu_operands(*dev)
+    out1 = torch.full((1, 8, 1024, 64), float("nan"), device="cuda")
+    fa.forward_mxfp4(*ops, out=out1)
+    out2 = torch.full_like(out1, float("nan"))
+    fa.forward_mxfp4(*ops, out=out2)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out1).all()
+    assert torch.equal(out1, out2)
+
+
+def test_bf16_output_is_rounded_fp32_output(fa):
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    ops = gpu_operands(*dev)
+    o32 = fa.forward_mxfp4(*ops)
+    o16 = fa.forward_mxfp4(*ops, out_dtype=torch.bfloat16)
+    assert torch.equal(o16, o32.to(torch.bfloat16))
+
+
+def test_error_paths_do_not_launch(fa):
+    host64, dev = load_workload("tiny_b1h1_n128_d64")
+    ops = gpu_operands(*dev)
+    out = torch.full((1, 1, 128, 64), 7.0, device="cuda")
+    lib = fa.lib
+    import ctypes
+    p = [ctypes.c_void_p(t.data_ptr()) for t in ops]
+    o = ctypes.c_void_p(out.data_ptr())
+    assert lib.fp4attn_forward_mxfp4(*p, 1, 1, 96, 64, 0.125, 1.5, 1.2, o, 0, None) == 1   # N not /128
+    assert lib.fp4attn_forward_mxfp4(*p, 1, 1, 128, 96, 0.125, 1.5, 1.2, o, 0, None) == 2  # d unsupported
+    assert lib.fp4attn_forward_mxfp4(*p, 1, 1, 128, 64, -1.0, 1.5, 1.2, o, 0, None) == 1   # bad scale
+    assert lib.fp4attn_forward_mxfp4(*p, 1, 1, 128, 64, 0.125, 0.0, 1.2, o, 0, None) == 1  # bad A
+    assert lib.fp4attn_forward_mxfp4(*p, 1, 1, 128, 64, 0.125, 1.5, 1.2, o, 5, None) == 1  # bad dtype
+    bad = ctypes.c_void_p(out.data_ptr() + 4)
+    assert lib.fp4attn_forward_mxfp4(*p, 1, 1, 128, 64, 0.125, 1.5, 1.2, bad, 0, None) == 1  # misaligned
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+    with pytest.raises(fa.Fp4AttnError):
+        fa.forward_mxfp4(*ops, softmax_scale=float("inf"))

@@ -1,0 +1,90 @@
+"""GPU parity of the MXFP4 quantizer: bit-exact codes and E8M0 bytes against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import mxfp4
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fa():
+    import paper_2609_04105_amd as fa
+    return fa
+
+
+def _check(fa, x_cpu, axis):
+    cg, sg = fa.quantize_mxfp4(x_cpu.cuda(), axis=axis)
+    co, so = mxfp4.quantize(workloads.as_f64(x_cpu), axis=axis)
+    assert np.array_equal(sg.cpu().numpy(), so), "scale bytes differ"
+    assert np.array_equal(cg.cpu().numpy(), co), "code bytes differ"
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("axis", [-1, -2])
+def test_ragged_random(fa, dtype, axis):
+    # 3 x 96 x 160: 1440 (axis -1) or 1440 (axis -2) blocks, not a multiple of the 256-thread launch
+    g = torch.Generator().manual_seed(100)
+    x = (torch.randn(3, 96, 160, generator=g) * torch.exp2(torch.randint(-6, 6, (3, 96, 160), generator=g))).to(dtype)
+    _check(fa, x, axis)
+
+
+@pytest.mark.parametrize("axis", [-1, -2])
+def test_adversarial_blocks(fa, axis):
+    blocks = []
+    mags = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+    blocks.append(torch.cat([mags, -mags, mags / 6 * 4, -mags / 3]))                # exact table values
+    mids = torch.tensor([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0])
+    blocks.append(torch.cat([mids, mids / 2, -mids / 4, mids * 2 / 3]))             # rounding ties
+    blocks.append(torch.zeros(32))                                                  # zero block
+    z = torch.zeros(32)
+    z[3] = -0.0
+    blocks.append(z)                                                                # signed zero
+    blocks.append(torch.full((32,), 2.0 ** -140))                                   # below E8M0 range
+    blocks.append(torch.full((32,), 3.0e38))                                        # near fp32 max
+    w = torch.ones(32)
+    w[0] = 2.0 ** 30
+    blocks.append(w * torch.linspace(-1, 1, 32))                                    # wide dynamic range
+    nan = torch.randn(32, generator=torch.Generator().manual_seed(1))
+    nan[5] = float("nan")
+    blocks.append(nan)
+    inf = torch.randn(32, generator=torch.Generator().manual_seed(2))
+    inf[9] = float("inf")
+    blocks.append(inf)
+    g = torch.Generator().manual_seed(3)
+    for _ in range(23):
+        blocks.append(torch.randn(32, generator=g) * float(2.0 ** torch.randint(-20, 20, (1,), generator=g)))
+    x = torch.stack(blocks)                   # [32 blocks, 32]
+    if axis == -2:
+        x = x.T.contiguous()                  # blocks along rows
+    _check(fa, x.to(torch.float32).reshape(1, *x.shape), axis)
+
+
+@pytest.mark.parametrize("name", list(workloads.WORKLOADS))
+def test_workload_operands(fa, name):
+    """Bit-exact on the workloads: every block for small ones; for large ones the
+    sampled query rows of Q and K and two full heads of V."""
+    w = workloads.WORKLOADS[name]
+    q, k, v = workloads.generate(w)
+    qg, kg, vg = q.cuda(), k.cuda(), v.cuda()
+    ops = fa.quantize_qkv(qg, kg, vg)
+    host = [t.cpu().numpy() for t in ops]
+    if w.all_rows:
+        qc, qs = mxfp4.quantize(workloads.as_f64(q), axis=-1)
+        kc, ks = mxfp4.quantize(workloads.as_f64(k), axis=-1)
+        vc, vs = mxfp4.quantize(workloads.as_f64(v), axis=-2)
+        for got, ref in zip(host, (qc, qs, kc, ks, vc, vs)):
+            assert np.array_equal(got, ref)
+        return
+    rows = workloads.sampled_rows(w)
+    b, h, i = rows // (w.H * w.N), (rows // w.N) % w.H, rows % w.N
+    for x, cg, sg in ((q, host[0], host[1]), (k, host[2], host[3])):
+        x64 = workloads.as_f64(x[torch.from_numpy(b), torch.from_numpy(h), torch.from_numpy(i)])
+        c_ref, s_ref = mxfp4.quantize(x64, axis=-1)
+        assert np.array_equal(cg[b, h, i], c_ref) and np.array_equal(sg[b, h, i], s_ref)
+    for bh in (0, w.B * w.H - 1):
+        bb, hh = divmod(bh, w.H)
+        c_ref, s_ref = mxfp4.quantize(workloads.as_f64(v[bb, hh]), axis=-2)
+        assert np.array_equal(host[4][bb, hh], c_ref) and np.array_equal(host[5][bb, hh], s_ref)

@@ -68,3 +68,15 @@ def test_rejects_negative_and_nan():
         e2m1.round_index(-1.0)
     with pytest.raises(ValueError):
         e2m1.round_index(np.nan)
+
+
+def test_round_matches_exhaustive_nearest_entry():
+    """Brute force: distance to all eight magnitudes, ties to the even index."""
+    rng = np.random.default_rng(9)
+    r = np.concatenate([rng.uniform(0, 7, 50000), e2m1.MAGNITUDES,
+                        (e2m1.MAGNITUDES[1:] + e2m1.MAGNITUDES[:-1]) / 2])
+    dist = np.abs(r[:, None] - e2m1.MAGNITUDES[None, :])
+    best = dist == dist.min(axis=1, keepdims=True)
+    even = np.arange(8) % 2 == 0
+    want = np.where(best.sum(axis=1) > 1, np.argmax(best & even, axis=1), np.argmax(best, axis=1))
+    assert np.array_equal(e2m1.round_index(r), want)
