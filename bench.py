@@ -110,6 +110,9 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
+    ap.add_argument("--traffic-run", action="store_true",
+                    help="for rocprofv3 --pmc passes: one 256 MiB device copy (counter calibration), "
+                         "then one forward launch; prints no JSON")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the forward shards over (batch, head) with no communication "
@@ -132,6 +135,17 @@ def main():
     q16, k16 = q.to(torch.bfloat16), k.to(torch.bfloat16)
     vt16 = fa.transpose_bf16(v.to(torch.bfloat16))
     out16 = torch.empty_like(out)
+
+    if args.traffic_run:
+        src = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)                      # reads and writes exactly 256 MiB
+        torch.cuda.synchronize()
+        fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out)
+        torch.cuda.synchronize()
+        print(f"traffic run done: copy 268435456 B, one forward on {name}", flush=True)
+        return
 
     def fp4_step():
         fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out)
