@@ -66,8 +66,7 @@ typedef enum {
  *
  * Errors: INVALID_ARG if a pointer is null or misaligned, batch < 1, rows < 1,
  * cols < 1, the blocked extent (cols for axis 1, rows for axis 0) is not a
- * multiple of 32, the other extent is odd for axis 0 (codes pack two per byte),
- * axis is not 0 or 1, or src_dtype is not a fp4attn_dtype.
+ * multiple of 32, axis is not 0 or 1, or src_dtype is not a fp4attn_dtype.
  * The quantizer is not part of the timed forward (the paper times the kernel
  * on prequantized operands).
  */
@@ -98,7 +97,8 @@ fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t ba
  * Errors: INVALID_ARG for null/misaligned pointers, B < 1, H < 1, N < 128 or
  * N % 128 != 0, softmax_scale not finite or <= 0, affine_a not finite or <= 0,
  * affine_b not finite, bad out_dtype, or B*H*N beyond 2^31.  UNSUPPORTED for
- * d not in {64, 128}.  NaN inputs propagate to the affected rows.
+ * d not in {64, 128}.  Non-finite operands (E8M0 byte 255) give unspecified but
+ * non-faulting results for the rows they touch.
  */
 fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales,
                                      const uint8_t* k_codes, const uint8_t* k_scales,

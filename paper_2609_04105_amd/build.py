@@ -15,6 +15,9 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libfp4attn.so")
 SOURCES = ["api.hip", "quantize.hip", "fwd_mxfp4.hip", "fwd_bf16.hip"]
+# The attention kernels never rely on NaN ordering in fmax; without this flag the
+# compiler canonicalizes every fmax operand with an extra v_max_f32.
+EXTRA = {"fwd_mxfp4.hip": ["-fno-honor-nans"], "fwd_bf16.hip": ["-fno-honor-nans"]}
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -32,7 +35,7 @@ FLAGS = [
 
 def _compile(src):
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     err = "\n".join(l for l in res.stderr.splitlines() if "packed-fp32-ops" not in l)
     if res.returncode != 0:

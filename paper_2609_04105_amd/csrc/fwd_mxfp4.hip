@@ -26,9 +26,9 @@
 //   v_cvt_scalef32_pk_fp4_f32 with scale 1/8 (two scores per instruction);
 //   the clamp to [0, 1] realises max(0, u) and saturation for free, and scaling
 //   by a power of two leaves every rounding decision unchanged.
-// - Denominator c_B: an extra 32x32x64 product of the same P^T operand with a
-//   constant "ones" row, so it uses exactly the codes and E8M0 bytes of PV and
-//   costs no vector-ALU work.
+// - Denominator c_B: an extra 16x16x128 product of the same P^T register with a
+//   constant indicator operand, so it uses exactly the codes and E8M0 bytes of
+//   PV and costs no vector-ALU work (half a 32x32x64 product per 64 keys).
 // - K/V tiles of 128 keys are staged in LDS in matrix-operand order (each
 //   lane's 16-byte fragment contiguous), double-buffered through registers.
 // - Workgroups are remapped so that the query tiles of one head run on one XCD
@@ -42,6 +42,7 @@ namespace {
 
 constexpr int kBN = 128;   // keys per LDS tile
 constexpr int kTau = 8;    // lazy rescale: the reference may lag the row maximum by up to 8 binades
+constexpr int kStages = 4; // LDS ring depth in tiles
 constexpr double kLog2E = 1.4426950408889634;
 constexpr double kLog2Of6 = 2.584962500721156;
 
@@ -79,6 +80,16 @@ struct Layout {
 // Key of operand row m (0..31) within a 32-key block, and its inverse.
 __device__ __forceinline__ int key_of_row(int m) { return 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3); }
 __device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * (k >> 4) + (k & 3); }
+
+template <int D, int NW>
+struct TileRegs;
+
+// Placeholder for an unused staging set.
+template <int D>
+struct TileRegs<D, 0> {
+  __device__ __forceinline__ void load(const uint8_t*, const uint8_t*, const uint8_t*, const uint8_t*, int, int, int) {}
+  __device__ __forceinline__ void store(uint8_t*, int) const {}
+};
 
 template <int D, int NW>
 struct TileRegs {
@@ -153,7 +164,7 @@ template <int D, int NW, bool DUMP, bool OUT_BF16>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_mxfp4_kernel(const KParams p) {
   using L = Layout<D>;
   constexpr int BM = NW * 32;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * L::stage];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * L::stage];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, lr = lane & 31;
@@ -197,124 +208,194 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
   }
 
-  const int ones_word = lr == 0 ? 0x22222222 : 0;  // E2M1 1.0 in every nibble of row 0
+  // Denominator operand.  Read as the B operand of a 16x16x128 product, the K64
+  // P^T register of lane l is column l % 16 and K-block l / 16, i.e. query
+  // (l % 32)'s keys 32 (l / 32) .. +31.  Row 0 of this indicator matrix selects
+  // K-blocks 0 and 2 (query c's 64 keys), row 1 K-blocks 1 and 3 (query c + 16),
+  // so one 16x16x128 product yields every query's code sum with the P scales.
+  const int ones_word = (lane == 0 || lane == 32 || lane == 17 || lane == 49) ? 0x22222222 : 0;  // E2M1 1.0
   const v4i ones = {ones_word, ones_word, ones_word, ones_word};
 
   v16f O[D / 32];
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) O[c] = v16f{};
-  v16f Dacc = v16f{};
+  v4f Dacc = v4f{};  // lane c < 16: register 0 = query c, register 1 = query c + 16
   int Mref = -(1 << 20);  // no block seen yet
 
-  TileRegs<D, NW> regs;
-  regs.load(kc, ks, vc, vs, N, 0, tid);
-  regs.store(lds, tid);
+  const int ntiles = N / kBN;
+  const int nsteps = 2 * ntiles;  // 64-key steps
+
+  // S^T of 64-key step `sl` (0 or 1) of the tile held in `st`: two 32-key blocks.
+  auto qk = [&](const uint8_t* st, auto SL_, v16f(&acc)[2]) {
+    constexpr int sl = decltype(SL_)::value;
+    static_for<2>([&](auto T_) {
+      constexpr int t = decltype(T_)::value;
+      constexpr int sub = 2 * sl + t;
+      v16f a = v16f{};
+      const int ksc = reinterpret_cast<const int*>(st + L::ksOff)[sub * 64 + lane];
+      static_for<D / 64>([&](auto C_) {
+        constexpr int c = decltype(C_)::value;
+        const v4i kf = *reinterpret_cast<const v4i*>(st + L::kOff + ((sub * (D / 64) + c) * 64 + lane) * 16);
+        a = mfma_fp4_32x32x64<2 * c, 2 * c>(kf, qf[c], a, ksc, qsc);
+      });
+      acc[t] = a;
+    });
+  };
+
+  // PV of step `s` (0 or 1) of the tile held in `st`, and the represented
+  // denominator from the same P^T operand and E8M0 bytes.
+  auto pv = [&](const uint8_t* st, auto S_, const v4i& P, int u) {
+    constexpr int s = decltype(S_)::value;
+    static_for<D / 32>([&](auto C_) {
+      constexpr int c = decltype(C_)::value;
+      const v4i vf = *reinterpret_cast<const v4i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 16);
+      const int vsc = reinterpret_cast<const int*>(st + L::vsOff)[c * 64 + lane];
+      O[c] = mfma_fp4_32x32x64<2 * s, 0>(vf, P, O[c], vsc, u);
+    });
+    Dacc = mfma_fp4_16x16x128<0, 0>(ones, P, Dacc, 127, u);
+  };
+
+  // Direct-P for global 64-key step g (Alg. 2, steps 1-6) on its S^T blocks:
+  // codes -> P (the K64 P^T operand), then the row reference and the E8M0 byte.
+  // The codes do not depend on the row reference, so the rare rescale branch
+  // comes last and the code map shares one basic block with the matrix work.
+  auto directp = [&](const v16f(&acc)[2], int g, v4i& P, int& u) {
+    float m0 = acc[0][0], m1 = acc[1][0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) {
+      m0 = fmaxf(m0, acc[0][r]);
+      m1 = fmaxf(m1, acc[1][r]);
+    }
+    unsigned xa = as_uint(m0), xb = as_uint(m1);
+    swap_halves(xa, xb);  // lower: (own m0, partner m0); upper: (partner m1, own m1)
+    const float mx = fmaxf(as_float(xa), as_float(xb));
+    unsigned ya = as_uint(mx), yb = ya;
+    swap_halves(ya, yb);  // every lane: (block-0 max, block-1 max)
+    const float E0 = floorf(as_float(ya) * p.c_y);
+    const float E1 = floorf(as_float(yb) * p.c_y);
+    const float c00 = fmaf(-p.a8, E0, p.k0_8);
+    const float c01 = fmaf(-p.a8, E1, p.k0_8);
+    // Every byte of X0..Y1 is written by the four converts below; the first
+    // convert of each word takes its own first input as the (overwritten) old
+    // value, so no register has to be cleared.
+    unsigned X0, X1, Y0, Y1;
+    static_for<4>([&](auto I_) {
+      constexpr int i = decltype(I_)::value;
+      const float a0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i], c00), 0.0f, 1.0f);
+      const float a1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i + 1], c00), 0.0f, 1.0f);
+      const float a2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i], c00), 0.0f, 1.0f);
+      const float a3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i + 1], c00), 0.0f, 1.0f);
+      const float b0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i], c01), 0.0f, 1.0f);
+      const float b1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i + 1], c01), 0.0f, 1.0f);
+      const float b2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i], c01), 0.0f, 1.0f);
+      const float b3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i + 1], c01), 0.0f, 1.0f);
+      X0 = cvt_pk_fp4<i>(i == 0 ? as_uint(a0) : X0, a0, a1, 0.125f);
+      X1 = cvt_pk_fp4<i>(i == 0 ? as_uint(a2) : X1, a2, a3, 0.125f);
+      Y0 = cvt_pk_fp4<i>(i == 0 ? as_uint(b0) : Y0, b0, b1, 0.125f);
+      Y1 = cvt_pk_fp4<i>(i == 0 ? as_uint(b2) : Y1, b2, b3, 0.125f);
+    });
+    // Pair the two blocks into the K64 P^T operand: lower half <- block 0, upper <- block 1.
+    swap_halves(X0, Y0);
+    swap_halves(X1, Y1);
+    P = v4i{(int)X0, (int)X1, (int)Y0, (int)Y1};
+    const int E0i = (int)E0, E1i = (int)E1;
+    const int Enew = max(E0i, E1i);
+    const bool need = Enew > Mref + kTau;
+    if (__builtin_amdgcn_ballot_w64(need)) {
+      // lazy, exact power-of-two rescale of what PV has accumulated so far
+      const int Mn = need ? Enew : Mref;
+      const int sh = Mref - Mn;
+#pragma unroll
+      for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
+      Dacc[0] = ldexpf(Dacc[0], sh);
+      Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
+      Mref = Mn;
+    }
+    const int Eown = h ? E1i : E0i;
+    u = min(max(Eown - Mref + 127, 0), 254);
+    if constexpr (DUMP) {
+      if (slot >= 0) {
+        const int kb = 2 * g + h;
+        *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
+        p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)Eown;
+      }
+    }
+  };
+
+  // Pipeline.  LDS holds a ring of kStages = 4 tiles; at the start of tile t the
+  // staged registers of tile t+1 are published and tile t+3 is fetched into the
+  // freed register set (two sets: even and odd tiles).  In 64-key step g the
+  // matrix unit runs PV of step g and QK of step g+2 while the vector ALU runs
+  // Direct-P of step g+1.  Steps are unrolled eight at a time (four tiles), so
+  // every LDS offset and register set is a compile-time constant.
+  // With four waves each thread stages twice the bytes, so only one set is kept
+  // and tiles are fetched two (not three) tiles ahead.
+  constexpr bool kTwoSets = NW == 8;
+  constexpr int kAhead = kTwoSets ? 3 : 2;
+  TileRegs<D, NW> st_even;
+  TileRegs<D, kTwoSets ? NW : 0> st_odd;
+  st_even.load(kc, ks, vc, vs, N, 0, tid);
+  st_even.store(lds, tid);
+  if constexpr (kTwoSets) {
+    if (ntiles > 1) st_odd.load(kc, ks, vc, vs, N, kBN, tid);
+    if (ntiles > 2) st_even.load(kc, ks, vc, vs, N, 2 * kBN, tid);
+  } else {
+    if (ntiles > 1) st_even.load(kc, ks, vc, vs, N, kBN, tid);
+  }
   __syncthreads();
 
-  const int ntiles = N / kBN;
-  for (int kt = 0; kt < ntiles; ++kt) {
-    uint8_t* st = lds + (kt & 1) * L::stage;
-    if (kt + 1 < ntiles) regs.load(kc, ks, vc, vs, N, (kt + 1) * kBN, tid);
-    const int key0 = kt * kBN;
+  // Two S^T buffers and two P operands alternate with the step parity.
+  v16f SA[2], SB[2];
+  v4i PA, PB;
+  int uA, uB;
+  qk(lds, std::integral_constant<int, 0>{}, SA);
+  directp(SA, 0, PA, uA);
+  qk(lds, std::integral_constant<int, 1>{}, SA);
 
-    static_for<kBN / 64>([&](auto S_) {
-      constexpr int s = decltype(S_)::value;
-      // S^T for the two 32-key blocks of this 64-key step.
-      v16f acc[2];
-      static_for<2>([&](auto T_) {
-        constexpr int sub = 2 * s + decltype(T_)::value;
-        v16f a = v16f{};
-        const int ksc = reinterpret_cast<const int*>(st + L::ksOff)[sub * 64 + lane];
-        static_for<D / 64>([&](auto C_) {
-          constexpr int c = decltype(C_)::value;
-          const v4i kf = *reinterpret_cast<const v4i*>(st + L::kOff + ((sub * (D / 64) + c) * 64 + lane) * 16);
-          a = mfma_fp4_32x32x64<2 * c, 2 * c>(kf, qf[c], a, ksc, qsc);
-        });
-        acc[decltype(T_)::value] = a;
-      });
+  // One step of the pipeline; j is the step's position in its group of eight.
+  // GUARD: the tail group, where QK, Direct-P or the step itself may not exist.
+  auto step = [&](auto J_, auto GUARD_, int g) {
+    constexpr int j = decltype(J_)::value;
+    constexpr bool guard = decltype(GUARD_)::value;
+    constexpr int sl = j % 2;                 // step within its tile
+    constexpr int b_cur = (j / 2) % kStages;  // ring slot of tile t
+    constexpr int b_nxt = (j / 2 + 1) % kStages;
+    auto& S_in = (sl == 0) ? SA : SB;   // S^T of step g+1
+    auto& S_out = (sl == 0) ? SB : SA;  // S^T of step g+2
+    auto& P_cur = (sl == 0) ? PA : PB;  // P of step g
+    auto& u_cur = (sl == 0) ? uA : uB;
+    auto& P_nxt = (sl == 0) ? PB : PA;  // P of step g+1
+    auto& u_nxt = (sl == 0) ? uB : uA;
+    const int t = g >> 1;
+    if constexpr (sl == 0) {
+      auto publish = [&](auto& set) {  // `set` holds tile t+1
+        if (!guard || t + 1 < ntiles) set.store(lds + b_nxt * L::stage, tid);
+        __syncthreads();
+        if (t + kAhead < ntiles) set.load(kc, ks, vc, vs, N, (t + kAhead) * kBN, tid);
+      };
+      if constexpr (kTwoSets && (j / 2) % 2 == 0) publish(st_odd);
+      else publish(st_even);
+    }
+    pv(lds + b_cur * L::stage, std::integral_constant<int, sl>{}, P_cur, u_cur);
+    if (!guard || g + 2 < nsteps) qk(lds + b_nxt * L::stage, std::integral_constant<int, sl>{}, S_out);
+    if (!guard || g + 1 < nsteps) directp(S_in, g + 1, P_nxt, u_nxt);
+  };
 
-      // Block maxima (Alg. 2, step 1): 16 scores per lane, then across halves.
-      float m0 = acc[0][0], m1 = acc[1][0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) {
-        m0 = fmaxf(m0, acc[0][r]);
-        m1 = fmaxf(m1, acc[1][r]);
-      }
-      unsigned xa = as_uint(m0), xb = as_uint(m1);
-      swap_halves(xa, xb);  // lower: (own m0, partner m0); upper: (partner m1, own m1)
-      const float mx = fmaxf(as_float(xa), as_float(xb));
-      unsigned ya = as_uint(mx), yb = ya;
-      swap_halves(ya, yb);  // every lane: (block-0 max, block-1 max)
-      // Block exponents (step 2).
-      const float E0 = floorf(as_float(ya) * p.c_y);
-      const float E1 = floorf(as_float(yb) * p.c_y);
-      const int E0i = (int)E0, E1i = (int)E1;
-      // Online integer reference with a lazy, exact power-of-two rescale.
-      const int Enew = max(E0i, E1i);
-      const bool need = Enew > Mref + kTau;
-      if (__builtin_amdgcn_ballot_w64(need)) {
-        const int Mn = need ? Enew : Mref;
-        const int sh = Mref - Mn;
-#pragma unroll
-        for (int c = 0; c < D / 32; ++c)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
-        Dacc[0] = ldexpf(Dacc[0], sh);
-        Mref = Mn;
-      }
-      const int u0 = min(max(E0i - Mref + 127, 0), 254);
-      const int u1 = min(max(E1i - Mref + 127, 0), 254);
-      const int ulane = h ? u1 : u0;
-      // Code map (steps 3-4) on u / 8.
-      const float c00 = fmaf(-p.a8, E0, p.k0_8);
-      const float c01 = fmaf(-p.a8, E1, p.k0_8);
-      unsigned X0 = 0, X1 = 0, Y0 = 0, Y1 = 0;
-      static_for<4>([&](auto I_) {
-        constexpr int i = decltype(I_)::value;
-        const float a0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i], c00), 0.0f, 1.0f);
-        const float a1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i + 1], c00), 0.0f, 1.0f);
-        const float a2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i], c00), 0.0f, 1.0f);
-        const float a3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i + 1], c00), 0.0f, 1.0f);
-        const float b0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i], c01), 0.0f, 1.0f);
-        const float b1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i + 1], c01), 0.0f, 1.0f);
-        const float b2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i], c01), 0.0f, 1.0f);
-        const float b3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i + 1], c01), 0.0f, 1.0f);
-        X0 = cvt_pk_fp4<i>(X0, a0, a1, 0.125f);
-        X1 = cvt_pk_fp4<i>(X1, a2, a3, 0.125f);
-        Y0 = cvt_pk_fp4<i>(Y0, b0, b1, 0.125f);
-        Y1 = cvt_pk_fp4<i>(Y1, b2, b3, 0.125f);
-      });
-      // Pair the two blocks into the K64 P^T operand: lower half <- block 0, upper <- block 1.
-      swap_halves(X0, Y0);
-      swap_halves(X1, Y1);
-      const v4i P = {(int)X0, (int)X1, (int)Y0, (int)Y1};
-
-      if constexpr (DUMP) {
-        if (slot >= 0) {
-          const int kb = (key0 + 64 * s) / 32 + h;
-          *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
-          p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)(h ? E1i : E0i);
-        }
-      }
-
-      // PV (step 6 numerator) and the represented denominator from the same operand.
-      static_for<D / 32>([&](auto C_) {
-        constexpr int c = decltype(C_)::value;
-        const v4i vf = *reinterpret_cast<const v4i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 16);
-        const int vsc = reinterpret_cast<const int*>(st + L::vsOff)[c * 64 + lane];
-        O[c] = mfma_fp4_32x32x64<2 * s, 0>(vf, P, O[c], vsc, ulane);
-      });
-      Dacc = mfma_fp4_32x32x64<0, 0>(ones, P, Dacc, 127, ulane);
-    });
-
-    if (kt + 1 < ntiles) regs.store(lds + ((kt + 1) & 1) * L::stage, tid);
-    __syncthreads();
+  int g0 = 0;
+  for (; g0 + 8 <= nsteps - 2; g0 += 8) {
+    static_for<8>([&](auto J_) { step(J_, std::false_type{}, g0 + decltype(J_)::value); });
   }
+  // tail: at most nine steps remain (nsteps - 2 - g0 < 8)
+  static_for<10>([&](auto J_) {
+    const int g = g0 + decltype(J_)::value;
+    if (g < nsteps) step(J_, std::true_type{}, g);
+  });
 
   // Epilogue: O = acc / (6 D).  The denominator sits in register 0 of the lower half.
-  unsigned d0 = as_uint(Dacc[0]), d1 = d0;
-  swap_halves(d0, d1);
-  const float Dfin = as_float(d0);
+  const float d_lo = lane_read(Dacc[0], lane & 15), d_hi = lane_read(Dacc[1], lane & 15);
+  const float Dfin = (lane & 16) ? d_hi : d_lo;  // query lane % 32
   const float inv = 1.0f / (6.0f * Dfin);
   const size_t orow = ((size_t)bh * N + qrow) * D;
 #pragma unroll

@@ -44,6 +44,23 @@ __device__ __forceinline__ v16f mfma_fp4_32x32x64(v4i a, v4i b, v16f c, int scal
                                                           OPSEL_B, scale_b);
 }
 
+// D = A * B + C on the scaled FP4 matrix unit, 16x16x128 (A lane l: row l % 16,
+// k = 32 (l / 16) + [0, 32); B lane l: column l % 16, same k; C lane l, register
+// r: row 4 (l / 16) + r, column l % 16).
+template <int OPSEL_A, int OPSEL_B>
+__device__ __forceinline__ v4f mfma_fp4_16x16x128(v4i a, v4i b, v4f c, int scale_a, int scale_b) {
+  v8i a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0};
+  v8i b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a8, b8, c, kFmtFp4, kFmtFp4, OPSEL_A, scale_a,
+                                                           OPSEL_B, scale_b);
+}
+
+// Value of `v` in lane `src` (any lane), through the LDS crossbar.
+__device__ __forceinline__ float lane_read(float v, int src) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src * 4, __builtin_bit_cast(int, v)));
+}
+__device__ __forceinline__ int lane_read(int v, int src) { return __builtin_amdgcn_ds_bpermute(src * 4, v); }
+
 __device__ __forceinline__ v16f mfma_bf16_32x32x16(v4i a, v4i b, v16f c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a), __builtin_bit_cast(v8bf, b), c, 0, 0,
                                                  0);
