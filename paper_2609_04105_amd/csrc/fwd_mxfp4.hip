@@ -77,9 +77,16 @@ struct Layout {
   static constexpr int stage = vsOff + vScales;
 };
 
-// Key of operand row m (0..31) within a 32-key block, and its inverse.
-__device__ __forceinline__ int key_of_row(int m) { return 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3); }
-__device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * (k >> 4) + (k & 3); }
+// Key order of the S^T product.  Operand row m = 8 g + 4 h + i of QK subtile
+// `sub` (two subtiles per 64-key step) holds key 32 h + 16 (sub & 1) + 4 g + i of
+// step sub / 2.  With the 32x32 accumulator layout, lane half h then holds all
+// 32 keys of block h of the step, in key order, in the two subtiles' registers.
+__device__ __forceinline__ int key_of_row(int sub, int m) {
+  return 64 * (sub >> 1) + 32 * ((m >> 2) & 1) + 16 * (sub & 1) + 4 * (m >> 3) + (m & 3);
+}
+// Inverse: (subtile, operand row) of key k of a 128-key tile.
+__device__ __forceinline__ int sub_of_key(int k) { return 2 * (k >> 6) + ((k >> 4) & 1); }
+__device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * ((k >> 5) & 1) + (k & 3); }
 
 template <int D, int NW>
 struct TileRegs;
@@ -110,7 +117,7 @@ struct TileRegs {
       if (nK % NT == 0 || slot < nK) {
         const int m = slot & 63, rest = slot >> 6;
         const int c = rest % (D / 64), sub = rest / (D / 64);
-        const int key = sub * 32 + key_of_row(m & 31);
+        const int key = key_of_row(sub, m & 31);
         const int j = 2 * c + (m >> 5);
         k[i] = *reinterpret_cast<const v4i*>(kc + (size_t)(key0 + key) * (D / 2) + j * 16);
       }
@@ -147,7 +154,7 @@ struct TileRegs {
       if (nV % NT == 0 || slot < nV) *reinterpret_cast<v4i*>(st + L::vOff + slot * 16) = v[i];
     }
     if (tid < kBN) {
-      const int sub = tid >> 5, m0 = row_of_key(tid & 31);
+      const int sub = sub_of_key(tid), m0 = row_of_key(tid);
       uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::ksOff) + sub * 64;
       dst[m0] = ks;            // lanes 0..31 use scale bytes 0, 2 (d blocks 0, 2)
       dst[m0 + 32] = ks >> 8;  // lanes 32..63 use bytes 1, 3
@@ -220,7 +227,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) O[c] = v16f{};
   v4f Dacc = v4f{};  // lane c < 16: register 0 = query c, register 1 = query c + 16
-  int Mref = -(1 << 20);  // no block seen yet
+  float Mref = -1.0e6f;  // integer row reference (exact in fp32); no block seen yet
 
   const int ntiles = N / kBN;
   const int nsteps = 2 * ntiles;  // 64-key steps
@@ -255,56 +262,60 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     Dacc = mfma_fp4_16x16x128<0, 0>(ones, P, Dacc, 127, u);
   };
 
-  // Direct-P for global 64-key step g (Alg. 2, steps 1-6) on its S^T blocks:
-  // codes -> P (the K64 P^T operand), then the row reference and the E8M0 byte.
-  // The codes do not depend on the row reference, so the rare rescale branch
-  // comes last and the code map shares one basic block with the matrix work.
-  auto directp = [&](const v16f(&acc)[2], int g, v4i& P, int& u) {
-    float m0 = acc[0][0], m1 = acc[1][0];
+  // Instruction order of one steady-state step (the region before the rescale
+  // branch): the step's LDS operand reads first, the block-maximum chain while
+  // they land, then every MFMA followed by a slice of the code map.
+  auto schedule_step = [&]() {
+    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);  // DS reads: V, K fragments and scales
+    __builtin_amdgcn_sched_group_barrier(0x002, 18, 0);  // VALU: block maximum, exponent, offset
+    static_for<D / 32 + 1 + 2 * (D / 64)>([&](auto) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // six VALU of the code map
+    });
+  };
+
+  // Direct-P for global 64-key step g (Alg. 2, steps 1-6).  Lane half h holds
+  // the 32 scores of block h of the step for query l % 32 (acc[0]: keys 0-15,
+  // acc[1]: keys 16-31), so the block maximum, the block exponent and the codes
+  // are all lane-local, and the codes land in the K64 P^T operand as they are
+  // converted.  Only the rare rescale branch exchanges the two halves' exponents.
+  auto directp = [&](const v16f(&acc)[2], int g, v4i& P, int& u, auto SCHED_) {
+    // 32 values in 16 three-input maxima (v_max3_f32)
+    float m = fmaxf(fmaxf(acc[0][0], acc[0][1]), acc[0][2]);
 #pragma unroll
-    for (int r = 1; r < 16; ++r) {
-      m0 = fmaxf(m0, acc[0][r]);
-      m1 = fmaxf(m1, acc[1][r]);
-    }
-    unsigned xa = as_uint(m0), xb = as_uint(m1);
-    swap_halves(xa, xb);  // lower: (own m0, partner m0); upper: (partner m1, own m1)
-    const float mx = fmaxf(as_float(xa), as_float(xb));
-    unsigned ya = as_uint(mx), yb = ya;
-    swap_halves(ya, yb);  // every lane: (block-0 max, block-1 max)
-    const float E0 = floorf(as_float(ya) * p.c_y);
-    const float E1 = floorf(as_float(yb) * p.c_y);
-    const float c00 = fmaf(-p.a8, E0, p.k0_8);
-    const float c01 = fmaf(-p.a8, E1, p.k0_8);
-    // Every byte of X0..Y1 is written by the four converts below; the first
-    // convert of each word takes its own first input as the (overwritten) old
-    // value, so no register has to be cleared.
-    unsigned X0, X1, Y0, Y1;
+    for (int r = 3; r < 15; r += 2) m = fmaxf(fmaxf(m, acc[0][r]), acc[0][r + 1]);
+    m = fmaxf(fmaxf(m, acc[0][15]), acc[1][0]);
+#pragma unroll
+    for (int r = 1; r < 15; r += 2) m = fmaxf(fmaxf(m, acc[1][r]), acc[1][r + 1]);
+    m = fmaxf(m, acc[1][15]);
+    const float E = floorf(m * p.c_y);          // block exponent (Alg. 2, step 2)
+    const float c0 = fmaf(-p.a8, E, p.k0_8);    // (A (log2 6 - E) + B) / 8
+    // Code map on u / 8.  Every byte of the four words is written below; the
+    // first convert of each word takes its own input as the overwritten value.
+    unsigned w[4];
     static_for<4>([&](auto I_) {
       constexpr int i = decltype(I_)::value;
-      const float a0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i], c00), 0.0f, 1.0f);
-      const float a1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][2 * i + 1], c00), 0.0f, 1.0f);
-      const float a2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i], c00), 0.0f, 1.0f);
-      const float a3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[0][8 + 2 * i + 1], c00), 0.0f, 1.0f);
-      const float b0 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i], c01), 0.0f, 1.0f);
-      const float b1 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][2 * i + 1], c01), 0.0f, 1.0f);
-      const float b2 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i], c01), 0.0f, 1.0f);
-      const float b3 = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[1][8 + 2 * i + 1], c01), 0.0f, 1.0f);
-      X0 = cvt_pk_fp4<i>(i == 0 ? as_uint(a0) : X0, a0, a1, 0.125f);
-      X1 = cvt_pk_fp4<i>(i == 0 ? as_uint(a2) : X1, a2, a3, 0.125f);
-      Y0 = cvt_pk_fp4<i>(i == 0 ? as_uint(b0) : Y0, b0, b1, 0.125f);
-      Y1 = cvt_pk_fp4<i>(i == 0 ? as_uint(b2) : Y1, b2, b3, 0.125f);
+      static_for<4>([&](auto W_) {
+        constexpr int wd = decltype(W_)::value;  // word wd holds keys 8 wd .. 8 wd + 7
+        const float lo = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[wd / 2][8 * (wd % 2) + 2 * i], c0), 0.0f, 1.0f);
+        const float hi = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[wd / 2][8 * (wd % 2) + 2 * i + 1], c0), 0.0f, 1.0f);
+        w[wd] = cvt_pk_fp4<i>(i == 0 ? as_uint(lo) : w[wd], lo, hi, 0.125f);
+      });
     });
-    // Pair the two blocks into the K64 P^T operand: lower half <- block 0, upper <- block 1.
-    swap_halves(X0, Y0);
-    swap_halves(X1, Y1);
-    P = v4i{(int)X0, (int)X1, (int)Y0, (int)Y1};
-    const int E0i = (int)E0, E1i = (int)E1;
-    const int Enew = max(E0i, E1i);
-    const bool need = Enew > Mref + kTau;
-    if (__builtin_amdgcn_ballot_w64(need)) {
-      // lazy, exact power-of-two rescale of what PV has accumulated so far
-      const int Mn = need ? Enew : Mref;
-      const int sh = Mref - Mn;
+    P = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+    // Keep the code map in this basic block, next to the step's matrix work,
+    // instead of letting it sink below the rescale branch (emits nothing).
+    asm volatile("" ::"v"(P));
+    if constexpr (decltype(SCHED_)::value) schedule_step();
+    // Online integer reference with a lazy, exact power-of-two rescale of what
+    // PV has accumulated so far; the halves agree on the reference because the
+    // branch is taken by the whole wave and uses both halves' exponents.
+    if (__builtin_amdgcn_ballot_w64(E > Mref + kTau)) {
+      unsigned ea = as_uint(E), eb = ea;
+      swap_halves(ea, eb);  // each lane: (block-0 exponent, block-1 exponent)
+      const float Emax = fmaxf(as_float(ea), as_float(eb));
+      const float Mn = Emax > Mref + kTau ? Emax : Mref;
+      const int sh = (int)(Mref - Mn);
 #pragma unroll
       for (int c = 0; c < D / 32; ++c)
 #pragma unroll
@@ -313,13 +324,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
       Mref = Mn;
     }
-    const int Eown = h ? E1i : E0i;
-    u = min(max(Eown - Mref + 127, 0), 254);
+    // E8M0 byte of this lane's block: clamp(E - M + 127, 0, 254) (E - M <= kTau).
+    u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mref + 127.0f, 0, 0u);
     if constexpr (DUMP) {
       if (slot >= 0) {
         const int kb = 2 * g + h;
         *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
-        p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)Eown;
+        p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)(int)E;
       }
     }
   };
@@ -351,7 +362,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   v4i PA, PB;
   int uA, uB;
   qk(lds, std::integral_constant<int, 0>{}, SA);
-  directp(SA, 0, PA, uA);
+  directp(SA, 0, PA, uA, std::false_type{});
   qk(lds, std::integral_constant<int, 1>{}, SA);
 
   // One step of the pipeline; j is the step's position in its group of eight.
@@ -379,9 +390,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       else publish(st_even);
     }
     pv(lds + b_cur * L::stage, std::integral_constant<int, sl>{}, P_cur, u_cur);
-    if (!guard || g + 2 < nsteps) qk(lds + b_nxt * L::stage, std::integral_constant<int, sl>{}, S_out);
-    if (!guard || g + 1 < nsteps) directp(S_in, g + 1, P_nxt, u_nxt);
+    if (!guard || g + 2 < nsteps) {
+      qk(lds + b_nxt * L::stage, std::integral_constant<int, sl>{}, S_out);
+      // Issue QK of step g+2 in this step (it would otherwise sink next to its
+      // consumer in step g+1 and serialise with the code map); emits nothing.
+      asm volatile("" ::"v"(S_out[0]), "v"(S_out[1]));
+    }
+    if (!guard || g + 1 < nsteps) directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
   };
+
 
   int g0 = 0;
   for (; g0 + 8 <= nsteps - 2; g0 += 8) {
@@ -417,7 +434,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   }
   if constexpr (DUMP) {
     if (slot >= 0 && h == 0) {
-      p.row_m[slot] = Mref;
+      p.row_m[slot] = (int)Mref;
       p.row_d[slot] = Dfin;
     }
   }
