@@ -26,13 +26,23 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 MXFP4_PEAK_TFLOPS = 10100.0   # MI355X dense FP4/FP6 matrix peak
 BF16_PEAK_TFLOPS = 2500.0     # MI355X dense BF16 matrix peak
 HBM_PEAK_GBS = 8000.0
+SPEC_CLOCK_GHZ = 2.4          # the clock the spec peaks assume
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_mxfp4_long_b1h32_n16384_d128_traffic.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_04105_amd", "csrc", "fwd_mxfp4.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_04105_amd", "csrc", f)
+                  for f in ("fwd_mxfp4.hip", "gfx950.hpp", "launch.hpp")]
 
 
 def _source_sha():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """Hash of the forward kernel's sources with comments and blank lines removed,
+    so that the committed counters stay attached to the code they measured."""
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path) as f:
+            for line in f:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
+    return h.hexdigest()
 
 
 def _traffic():
@@ -46,6 +56,60 @@ def _traffic():
     if t.get("source_sha256") != _source_sha():
         return None
     return t.get("bytes_per_launch")
+
+
+def traffic_summary(fetch_csv, write_csv, out_path=TRAFFIC_FILE):
+    """Write the per-launch HBM traffic file from the counter CSVs of two
+    ``--traffic-run`` passes (FETCH_SIZE, then WRITE_SIZE, in KiB per dispatch).
+    Each counter is scaled by what it reads for the 256 MiB device copy."""
+    import csv
+
+    def per_kernel(path, counter):
+        vals = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter:
+                    vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return vals
+
+    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+
+    def pick(vals, key):
+        hits = [v for k, v in vals.items() if key in k]
+        if len(hits) != 1 or len(hits[0]) != 1:
+            raise SystemExit(f"expected exactly one dispatch of {key!r} in the counter file, got {hits}")
+        return hits[0][0]
+
+    kname = "fwd_mxfp4_kernel<128, 8, false, false>"
+    copy_bytes = 256 << 20
+    fs = copy_bytes / 1024 / pick(fetch, "copyBuffer")
+    ws = copy_bytes / 1024 / pick(write, "copyBuffer")
+    fk, wk = pick(fetch, kname), pick(write, kname)
+    import workloads
+    w = workloads.WORKLOADS[workloads.BENCH_WORKLOAD]
+    algo = w.B * w.H * (3 * w.N * w.d * (0.5 + 1 / 32) + 4 * w.N * w.d)
+    res = {
+        "kernel": kname,
+        "workload": w.name,
+        "source_sha256": _source_sha(),
+        "fetch_size_kib": fk,
+        "write_size_kib": wk,
+        "copy_calibration": {"bytes": copy_bytes, "fetch_size_kib": pick(fetch, "copyBuffer"),
+                             "write_size_kib": pick(write, "copyBuffer"), "fetch_scale": fs, "write_scale": ws},
+        "fetch_bytes": fk * 1024 * fs,
+        "write_bytes": wk * 1024 * ws,
+        "bytes_per_launch": fk * 1024 * fs + wk * 1024 * ws,
+        "algorithmic_bytes": int(algo),
+        "commands": [
+            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <fetch> -o fetch -- python bench.py --traffic-run",
+            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write> -o write -- python bench.py --traffic-run",
+            "python bench.py --traffic-summary <fetch>/fetch_counter_collection.csv "
+            "<write>/write_counter_collection.csv",
+        ],
+    }
+    with open(out_path, "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res))
 
 
 def _time_windows(torch, fns, steps, windows):
@@ -64,6 +128,21 @@ def _time_windows(torch, fns, steps, windows):
             torch.cuda.synchronize()
             res[name].append(start.elapsed_time(end) / steps)
     return {k: sorted(v)[len(v) // 2] for k, v in res.items()}, res
+
+
+def measured_clock_ghz(torch, fa, ops, w, launches=5):
+    """Shader clock achieved by the timed forward kernel: launched through the
+    test entry point with no rows to dump (the plain forward kernel), each
+    workgroup records the shader-clock cycles and 100 MHz constant-clock ticks
+    of its residency; the ratio of the sums over workgroups and launches."""
+    no_rows = torch.zeros(0, dtype=torch.int64, device=ops[0].device)
+    cyc = ticks = 0
+    for _ in range(launches):
+        r = fa.debug_directp_mxfp4(*ops, no_rows, softmax_scale=w.softmax_scale, wg_clock=True)
+        c = r["wg_clock"].cpu()
+        cyc += int(c[:, 0].sum())
+        ticks += int(c[:, 1].sum())
+    return cyc / (ticks / 100e6) / 1e9
 
 
 def cpu_oracle_baseline(w, budget_s=12.0):
@@ -113,7 +192,12 @@ def main():
     ap.add_argument("--traffic-run", action="store_true",
                     help="for rocprofv3 --pmc passes: one 256 MiB device copy (counter calibration), "
                          "then one forward launch; prints no JSON")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the traffic file from the two --traffic-run counter CSVs (no GPU use)")
     args = ap.parse_args()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the forward shards over (batch, head) with no communication "
               "and nothing here uses a second GPU; run with --gpus 1", file=sys.stderr)
@@ -185,6 +269,8 @@ def main():
     tflops = flops / (fp4_ms * 1e-3) / 1e12
     bf16_tflops = flops / (med["bf16"] * 1e-3) / 1e12 if "bf16" in med else None
     traffic = _traffic()
+    clk = measured_clock_ghz(torch, fa, ops, w)
+    peak_clk = MXFP4_PEAK_TFLOPS * clk / SPEC_CLOCK_GHZ
     roof = {
         "bound": "mfma",
         "achieved": round(tflops, 2),
@@ -193,6 +279,9 @@ def main():
         "frac": round(tflops / MXFP4_PEAK_TFLOPS, 4),
         "traffic": traffic,
         "kernel": "fwd_mxfp4_kernel<128, 8, false, false>",
+        "measured_clock_ghz": round(clk, 3),
+        "peak_at_measured_clock": round(peak_clk, 1),
+        "frac_at_measured_clock": round(tflops / peak_clk, 4),
         "algorithmic_flops_per_launch": flops,
     }
     line = {

@@ -143,9 +143,19 @@ fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t ro
  *   block_exp  [n_rows, N/32] int16 absolute block exponents E_B
  *   row_m      [n_rows] int32 final integer row reference M_i
  *   row_d      [n_rows] fp32 represented denominator relative to 2^M_i
+ *   wg_clock   optional (NULL: not written), [B*H*N/128][2] uint64: workgroup
+ *              w of the launch writes entry [w][0], the shader-clock cycles
+ *              it was resident, and [w][1], the same interval in ticks of the
+ *              100 MHz constant clock; entries past the launch's workgroup
+ *              count (B*H*N/256 workgroups when 256-row tiles are used) are
+ *              left untouched.  Their ratio is the achieved shader clock.
  *
- * Errors: as fp4attn_forward_mxfp4, plus INVALID_ARG for n_rows < 1 or a null
- * dump pointer.
+ * With n_rows = 0 nothing is dumped (the five dump pointers are ignored and
+ * may be NULL) and the launch is the plain forward kernel itself, so wg_clock
+ * then records the clock of exactly the timed kernel.
+ *
+ * Errors: as fp4attn_forward_mxfp4, plus INVALID_ARG for n_rows < 0, a null
+ * dump pointer when n_rows > 0, or a wg_clock that is not 16-byte aligned.
  */
 fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales,
                                            const uint8_t* k_codes, const uint8_t* k_scales,
@@ -155,7 +165,8 @@ fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t
                                            void* out, int out_dtype,
                                            const int64_t* row_ids, int64_t n_rows,
                                            uint8_t* p_codes, int16_t* block_exp,
-                                           int32_t* row_m, float* row_d, void* stream);
+                                           int32_t* row_m, float* row_d, uint64_t* wg_clock,
+                                           void* stream);
 
 /* Static description of a status code; never NULL. */
 const char* fp4attn_status_string(int status);

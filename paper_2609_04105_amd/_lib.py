@@ -20,7 +20,7 @@ SIGNATURES = {
     "fp4attn_forward_bf16": [_c_p] * 3 + [_i64] * 4 + [_f32, _c_p, _int, _c_p],
     "fp4attn_transpose_bf16": [_c_p, _i64, _i64, _i64, _c_p, _c_p],
     "fp4attn_debug_directp_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32] * 3 + [_c_p, _int, _c_p, _i64]
-    + [_c_p] * 4 + [_c_p],
+    + [_c_p] * 5 + [_c_p],
     "fp4attn_status_string": [_int],
     "fp4attn_last_error": [],
     "fp4attn_abi_version": [],

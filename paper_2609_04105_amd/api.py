@@ -105,17 +105,19 @@ def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, sof
 
 
 def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, row_ids, softmax_scale=None,
-                        affine_a=1.5, affine_b=1.2, out_dtype=torch.float32):
+                        affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False):
     """Forward plus the Direct-P state of the (strictly ascending) flattened ``row_ids``.
 
     Returns a dict: out, p_codes [R, N/2] uint8, block_exp [R, N/32] int16,
-    row_m [R] int32, row_d [R] fp32.
+    row_m [R] int32, row_d [R] fp32, and with ``wg_clock`` also wg_clock
+    [B*H*N/128, 2] int64 (per workgroup: shader-clock cycles, 100 MHz ticks;
+    rows past the launch's workgroup count stay zero).
     """
     B, H, N, d = _fp4_shape(q_codes)
     ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
     _check_operands(B, H, N, d, ops)
     _need(row_ids, "row_ids", torch.int64, 1)
-    R = row_ids.numel()
+    R = row_ids.numel()   # 0: no dump, the launch is the plain forward kernel
     dev = q_codes.device
     out = torch.empty((B, H, N, d), dtype=out_dtype, device=dev)
     res = {
@@ -125,11 +127,13 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
         "row_m": torch.empty((R,), dtype=torch.int32, device=dev),
         "row_d": torch.empty((R,), dtype=torch.float32, device=dev),
     }
+    if wg_clock:
+        res["wg_clock"] = torch.zeros((B * H * N // 128, 2), dtype=torch.int64, device=dev)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
     check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
-                                          _DTYPES[out_dtype], _ptr(row_ids), R, _ptr(res["p_codes"]),
+                                          _DTYPES[out_dtype], _ptr(row_ids) if R else None, R, _ptr(res["p_codes"]),
                                           _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),
-                                          _stream(out)))
+                                          _ptr(res["wg_clock"]) if wg_clock else None, _stream(out)))
     return res
 
 

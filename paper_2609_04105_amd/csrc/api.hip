@@ -135,24 +135,30 @@ fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t
                                            const uint8_t* vt_scales, int64_t B, int64_t H, int64_t N, int64_t d,
                                            float softmax_scale, float affine_a, float affine_b, void* out,
                                            int out_dtype, const int64_t* row_ids, int64_t n_rows, uint8_t* p_codes,
-                                           int16_t* block_exp, int32_t* row_m, float* row_d, void* stream) {
+                                           int16_t* block_exp, int32_t* row_m, float* row_d, uint64_t* wg_clock,
+                                           void* stream) {
   const fp4attn_status st = check_directp(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
                                           softmax_scale, affine_a, affine_b, out, out_dtype);
   if (st != FP4ATTN_OK) return st;
-  REQUIRE_PTR(row_ids);
-  REQUIRE_PTR(p_codes);
-  REQUIRE_PTR(block_exp);
-  REQUIRE_PTR(row_m);
-  REQUIRE_PTR(row_d);
-  if (n_rows < 1 || n_rows > 0x7fffffff) return fail(FP4ATTN_ERR_INVALID_ARG, "n_rows must be in [1, 2^31)");
+  if (n_rows < 0 || n_rows > 0x7fffffff) return fail(FP4ATTN_ERR_INVALID_ARG, "n_rows must be in [0, 2^31)");
+  if (n_rows > 0) {
+    REQUIRE_PTR(row_ids);
+    REQUIRE_PTR(p_codes);
+    REQUIRE_PTR(block_exp);
+    REQUIRE_PTR(row_m);
+    REQUIRE_PTR(row_d);
+  }
   fp4attn::DirectPArgs a = directp_args(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
                                         softmax_scale, affine_a, affine_b, out, out_dtype);
-  a.row_ids = row_ids;
+  a.row_ids = n_rows > 0 ? row_ids : nullptr;
   a.n_rows = (int)n_rows;
   a.p_codes = p_codes;
   a.block_exp = block_exp;
   a.row_m = row_m;
   a.row_d = row_d;
+  if (wg_clock != nullptr && (reinterpret_cast<uintptr_t>(wg_clock) & 15) != 0)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "wg_clock is not 16-byte aligned");
+  a.wg_clock = reinterpret_cast<unsigned long long*>(wg_clock);
   return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "debug forward launch");
 }
 
@@ -202,6 +208,6 @@ const char* fp4attn_status_string(int status) {
 
 const char* fp4attn_last_error(void) { return g_last_error; }
 
-int fp4attn_abi_version(void) { return (1 << 16) | 0; }
+int fp4attn_abi_version(void) { return (1 << 16) | 1; }
 
 }  // extern "C"

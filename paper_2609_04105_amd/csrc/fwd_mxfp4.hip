@@ -15,22 +15,25 @@
 //   every accumulator, so the per-row online state (integer reference M_i, the
 //   lazy power-of-two rescale) is a per-lane scalar and needs no cross-lane
 //   broadcast.
-// - K rows are fed to the S^T product in the order pi(m) = 16 h + 4 g + i for
-//   operand row m = 8 g + 4 h + i.  With the 32x32 accumulator layout, lane half
-//   h then holds keys 16 h .. 16 h + 15 of each 32-key block in register order,
-//   so the E2M1 codes come out of the converter already in key order and one
-//   v_permlane32_swap per dword turns two adjacent blocks into the K64 P^T
-//   operand of the PV product (the paper's paired N32 -> K64 publication).
-// - Block maxima: 16 values per lane, then one half-wave exchange.
-// - Code map: one v_fma_f32 with the clamp modifier per score on u / 8, then
-//   v_cvt_scalef32_pk_fp4_f32 with scale 1/8 (two scores per instruction);
-//   the clamp to [0, 1] realises max(0, u) and saturation for free, and scaling
-//   by a power of two leaves every rounding decision unchanged.
+// - Keys are fed to the S^T product in a permuted order (key_of_row below)
+//   so that, with the 32x32 accumulator layout, lane half h holds all 32
+//   scores of N32 block h of each 64-key step, in key order, in the registers
+//   of two QK subtiles.  Block maximum, block exponent and E2M1 codes are then
+//   lane-local, and the converted codes already form the lane's K64 P^T operand
+//   of the PV product (the paper's two N32 fragments published as one K64
+//   operand) with no cross-lane data movement.
+// - Code map: one v_fma_f32 with the clamp modifier per score on u / 8 (the
+//   median with 0 and 1 folds into it), then v_cvt_scalef32_pk_fp4_f32 with
+//   scale 1/8 (two scores per instruction); the clamp realises max(0, u) and
+//   saturation, and scaling by a power of two changes no rounding decision.
 // - Denominator c_B: an extra 16x16x128 product of the same P^T register with a
 //   constant indicator operand, so it uses exactly the codes and E8M0 bytes of
-//   PV and costs no vector-ALU work (half a 32x32x64 product per 64 keys).
+//   PV and costs no vector-ALU work.
 // - K/V tiles of 128 keys are staged in LDS in matrix-operand order (each
-//   lane's 16-byte fragment contiguous), double-buffered through registers.
+//   lane's 16-byte fragment contiguous): a ring of four tiles, filled from
+//   registers that fetch two or three tiles ahead.  The key loop is software
+//   pipelined two deep: while the vector ALU maps step g+1 to codes, the
+//   matrix unit runs PV of step g and QK of step g+2.
 // - Workgroups are remapped so that the query tiles of one head run on one XCD
 //   and share its L2 copy of that head's K/V.
 #include "gfx950.hpp"
@@ -62,6 +65,7 @@ struct KParams {
   int16_t* block_exp;
   int32_t* row_m;
   float* row_d;
+  unsigned long long* wg_clock;
 };
 
 template <int D>
@@ -175,6 +179,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, lr = lane & 31;
+  const unsigned long long clk0 = __builtin_amdgcn_s_memtime(), rt0 = __builtin_amdgcn_s_memrealtime();
   const int lin = xcd_remap(blockIdx.x, p.total);
   const int bh = lin / p.n_qtiles, qt = lin % p.n_qtiles;
   const int N = p.N;
@@ -438,6 +443,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       p.row_d[slot] = Dfin;
     }
   }
+  if (p.wg_clock != nullptr && tid == 0) {
+    // shader-clock cycles and 100 MHz constant-clock ticks this workgroup was resident
+    const unsigned long long clk1 = __builtin_amdgcn_s_memtime(), rt1 = __builtin_amdgcn_s_memrealtime();
+    p.wg_clock[2 * blockIdx.x] = clk1 - clk0;
+    p.wg_clock[2 * blockIdx.x + 1] = rt1 - rt0;
+  }
 }
 
 template <int D, int NW, bool DUMP, bool OUT_BF16>
@@ -478,7 +489,8 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   kp.block_exp = a.block_exp;
   kp.row_m = a.row_m;
   kp.row_d = a.row_d;
-  const bool dump = a.row_ids != nullptr;
+  kp.wg_clock = a.wg_clock;
+  const bool dump = a.n_rows > 0;
   const int bh = a.B * a.H;
   // Eight waves (256 rows) per workgroup when that still fills the 256 CUs.
   const bool wide = (a.N % 256 == 0) && (int64_t)(a.N / 256) * bh >= 256;

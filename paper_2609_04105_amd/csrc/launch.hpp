@@ -32,6 +32,7 @@ struct DirectPArgs {
   int16_t* block_exp;
   int32_t* row_m;
   float* row_d;
+  unsigned long long* wg_clock;  // may be null
 };
 
 hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream);

@@ -78,4 +78,6 @@ def test_quantize_and_bf16_validation(lib):
     t = lib.fp4attn_transpose_bf16
     assert t(FAKE[0], 1, 7, 8, FAKE[1], None) == 1
     d = lib.fp4attn_debug_directp_mxfp4
-    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, FAKE[7], 0, *FAKE[:4], None) == 1
+    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, FAKE[7], -1, *FAKE[:4], None, None) == 1   # n_rows < 0
+    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, FAKE[7], 1, *FAKE[:4], ctypes.c_void_p(4096 + 8),
+             None) == 1                                                 # misaligned wg_clock

@@ -135,3 +135,25 @@ def test_error_paths_do_not_launch(fa):
     assert torch.all(out == 7.0)
     with pytest.raises(fa.Fp4AttnError):
         fa.forward_mxfp4(*ops, softmax_scale=float("inf"))
+
+
+@pytest.mark.parametrize("n_dump", [0, 1])
+@pytest.mark.parametrize("B,H,N,d,wgs", [(1, 2, 384, 128, 6), (1, 128, 512, 128, 256)])
+def test_workgroup_clock_record(fa, B, H, N, d, wgs, n_dump):
+    """The test entry point's per-workgroup clock record, with and without rows to
+    dump: exactly the launch's workgroups write it, with a plausible shader clock,
+    and the output equals the forward's."""
+    g = torch.Generator().manual_seed(11)
+    q, k, v = (torch.randn(B, H, N, d, generator=g).to(torch.bfloat16).cuda() for _ in range(3))
+    ops = gpu_operands(q, k, v)
+    print(f"[clock] B{B} H{H} N{N} d{d} dump rows {n_dump}", flush=True)
+    r = fa.debug_directp_mxfp4(*ops, torch.zeros(n_dump, dtype=torch.int64, device="cuda"), wg_clock=True)
+    out = fa.forward_mxfp4(*ops)
+    torch.cuda.synchronize()
+    assert torch.equal(out, r["out"])
+    c = r["wg_clock"].cpu()
+    assert c.shape == (B * H * N // 128, 2)
+    assert bool((c[:wgs] > 0).all()) and bool((c[wgs:] == 0).all())
+    ghz = float(c[:, 0].sum()) / (float(c[:, 1].sum()) / 100e6) / 1e9
+    print(f"[clock] {ghz:.3f} GHz", flush=True)
+    assert 0.3 < ghz < 3.0
