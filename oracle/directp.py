@@ -24,6 +24,15 @@ represented-contributions, represented-output):
    Other modes: ``affine64`` (the same map unfused in fp64), ``exp2`` (the ideal
    converter ``Q_E2M1(2**x)``, eq. ideal-code-path) and ``exp2_exact``
    (``2**x`` with no E2M1 rounding, used to check the normalisation).
+   Native-exponential mixing (Sec. "Fix 1": a selected pair may use the
+   native exponential; the balancing paragraph closing Sec. "Fix 2"; Table
+   policy-definition, ``accurate``; Table b300-tuning, EX2 density): with
+   ``ex2_pairs = k`` in {1, 2, 4, 8, 16}, pair p of each 32-key block (keys 2p
+   and 2p + 1, p = 0..15) takes the ideal converter instead of the affine map
+   when ``p % (16 / k) == 0``, i.e. k of the 16 pairs, evenly spaced.  Its fp32
+   decision folds the transform into one fma like the affine map:
+   ``x = fma(c_y, raw, c1_B)`` with ``c1_B = fp32(k1 - E_B)``,
+   ``k1 = fp32(log2 6)``, then ``q = Q_E2M1(fp32(2**x))``.
 4. Row reference: the paper's fast path is shiftless (m_i = 0).  Codes do not
    depend on the reference, so this oracle uses the integer reference
    ``M_i = max_B E_B`` and weights ``w_B = 2**(E_B - M_i)``; the E8M0 byte
@@ -51,6 +60,17 @@ LOG2_6 = 2.584962500721156
 
 BLOCK = 32
 MODES = ("affine32", "affine64", "exp2", "exp2_exact")
+EX2_PAIRS = (0, 1, 2, 4, 8, 16)
+
+
+def ex2_key_mask(ex2_pairs):
+    """[32] bool: the keys of a 32-key block whose code comes from ``2**x``
+    (pair p = key // 2 is selected iff p % (16 / ex2_pairs) == 0)."""
+    if ex2_pairs not in EX2_PAIRS:
+        raise ValueError(f"ex2_pairs must be one of {EX2_PAIRS}")
+    if ex2_pairs == 0:
+        return np.zeros(BLOCK, dtype=bool)
+    return (np.arange(BLOCK) // 2) % (16 // ex2_pairs) == 0
 
 
 def fp32_coefficients(softmax_scale, affine_a, affine_b):
@@ -78,14 +98,18 @@ def raw_scores(q6, k6):
     return raw
 
 
-def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affine32"):
+def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affine32", ex2_pairs=0):
     """(E [R, N/32] int64, q [R, N] fp64 magnitudes, k [R, N] uint8 code indices or None).
 
     ``raw`` is the [R, N] score matrix of step 1.  For ``exp2_exact`` the
     returned ``q`` holds the unrounded ``2**x`` and ``k`` is None.
+    ``ex2_pairs`` (mode ``affine32`` only) selects native-exponential mixing.
     """
     if mode not in MODES:
         raise ValueError(f"mode must be one of {MODES}")
+    mask = ex2_key_mask(ex2_pairs)
+    if ex2_pairs and mode != "affine32":
+        raise ValueError("ex2_pairs applies to the fp32 decision (mode affine32)")
     R, N = raw.shape
     if N % BLOCK:
         raise ValueError("key count must be a multiple of 32")
@@ -99,6 +123,13 @@ def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affi
         c0 = fp32.fma(-a32, E.astype(np.float32), k0)
         u = fp32.fma(c_a, raw32, np.repeat(c0, BLOCK, axis=-1)).astype(np.float64)
         k = e2m1.round_index(np.maximum(u, 0.0))
+        if ex2_pairs:
+            k1 = np.float32(LOG2_6)
+            c1 = fp32.fma(np.float32(-1.0), E.astype(np.float32), k1)       # fp32(k1 - E_B)
+            x = fp32.fma(c_y, raw32, np.repeat(c1, BLOCK, axis=-1))
+            p = np.exp2(x.astype(np.float64)).astype(np.float32).astype(np.float64)
+            keys = np.tile(mask, nb)
+            k = np.where(keys[None, :], e2m1.round_index(p), k)
         return E, e2m1.MAGNITUDES[k], k
     # fp64 modes follow eq. ideal-code-path / affine-code-map literally.
     s = float(np.float32(softmax_scale))
@@ -131,7 +162,7 @@ def _normalise(E, q, v6, M):
 
 def forward_rows(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, rows,
                  softmax_scale, affine_a=1.5, affine_b=1.2, mode="affine32",
-                 chunk=128, want_codes=True):
+                 chunk=128, want_codes=True, ex2_pairs=0):
     """Direct-P forward for the query ``rows`` of ONE (batch, head) slice.
 
     Operands are single-head MXFP4 arrays as produced by :func:`oracle.mxfp4.quantize`:
@@ -148,7 +179,7 @@ def forward_rows(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, rows
     out = {"E": [], "M": [], "D": [], "O": [], "codes": []}
     for lo in range(0, len(rows), chunk):
         raw = raw_scores(q6[lo:lo + chunk], k6)
-        E, q, k = block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode)
+        E, q, k = block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode, ex2_pairs)
         M = E.max(axis=-1)
         D, O = _normalise(E, q, v6, M)
         out["E"].append(E)
@@ -162,7 +193,7 @@ def forward_rows(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, rows
 
 
 def forward_rows_online(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, rows,
-                        softmax_scale, affine_a=1.5, affine_b=1.2, mode="affine32", tile=128):
+                        softmax_scale, affine_a=1.5, affine_b=1.2, mode="affine32", tile=128, ex2_pairs=0):
     """Online (tiled) form of :func:`forward_rows`: key tiles of width ``tile``.
 
     A running integer reference ``M`` starts at the first tile's maximum block
@@ -183,7 +214,7 @@ def forward_rows_online(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
     Es, codes = [], []
     for t0 in range(0, N, tile):
         raw = raw_scores(q6, k6[t0:t0 + tile])
-        E, q, k = block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode)
+        E, q, k = block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode, ex2_pairs)
         tile_max = E.max(axis=-1)
         M_new = tile_max if M is None else np.maximum(M, tile_max)
         rescale = np.ones(R) if M is None else np.ldexp(1.0, M - M_new)

@@ -214,3 +214,89 @@ def test_raw_scores_exactness_guard():
     k6 = np.array([[1.0, 2.0 ** -10]])
     with pytest.raises(ValueError):
         directp.raw_scores(q6, k6)   # 1 + 2**30 needs 31 significant bits
+
+
+# ---- native-exponential mixing (EX2 density) ----------------------------------------------
+
+def test_ex2_key_mask_spacing():
+    """k of the 16 pairs of a block, evenly spaced, both keys of a pair together."""
+    for kx in directp.EX2_PAIRS:
+        m = directp.ex2_key_mask(kx)
+        assert m.sum() == 2 * kx
+        assert np.array_equal(m[0::2], m[1::2])
+        if kx:
+            sel = np.flatnonzero(m[0::2])
+            assert np.all(np.diff(sel) == 16 // kx) and sel[0] == 0
+    with pytest.raises(ValueError):
+        directp.ex2_key_mask(3)
+
+
+@pytest.fixture(scope="module")
+def gaussian_head_d128():
+    rng = np.random.default_rng(20)
+    N, d = 1024, 128
+    (q, k, v), ops = _quantized_head(rng, N, d)
+    return (q, k, v), ops, 1 / np.sqrt(d)
+
+
+def test_all_ex2_pairs_is_the_ideal_converter(gaussian_head_d128):
+    """ex2_pairs = 16 decides every code as Q_E2M1(2**x) (eq. ideal-code-path); the
+    fp64 formula of that equation differs only where 2**x lies within fp32
+    rounding of an E2M1 boundary."""
+    _, ops, s = gaussian_head_d128
+    rows = np.arange(256)
+    mix = directp.forward_rows(*ops, rows, s, ex2_pairs=16)
+    ideal = directp.forward_rows(*ops, rows, s, mode="exp2_exact")     # unrounded 2**x, fp64
+    assert np.array_equal(mix["E"], ideal["E"])
+    p = ideal["codes"]
+    bounds = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0])
+    near = np.min(np.abs(p[..., None] / bounds - 1.0), axis=-1) < 1e-6
+    ref_codes = e2m1.round_index(p)
+    assert np.array_equal(mix["codes"][~near], ref_codes[~near])
+    # (the window holds, among others, every exactly-zero score of a block with
+    # E_B = 3: 2**x is then 6/8 = 0.75, a tie, where the fp64 formula's rounded
+    # log2 6 lands just below it)
+    assert near.mean() < 1e-3
+
+
+@pytest.mark.parametrize("kx", [1, 2, 4, 8])
+def test_ex2_mixing_touches_only_selected_pairs(gaussian_head_d128, kx):
+    """Unselected keys keep the affine codes bit for bit; selected keys carry the
+    all-native codes."""
+    _, ops, s = gaussian_head_d128
+    rows = np.arange(0, 1024, 5)
+    aff = directp.forward_rows(*ops, rows, s)["codes"]
+    nat = directp.forward_rows(*ops, rows, s, ex2_pairs=16)["codes"]
+    mix = directp.forward_rows(*ops, rows, s, ex2_pairs=kx)["codes"]
+    keys = np.tile(directp.ex2_key_mask(kx), mix.shape[1] // 32)
+    assert np.array_equal(mix[:, ~keys], aff[:, ~keys])
+    assert np.array_equal(mix[:, keys], nat[:, keys])
+    assert np.any(mix[:, keys] != aff[:, keys])
+
+
+def test_ex2_density_raises_fidelity(gaussian_head_d128):
+    """More native-exponential pairs move the operator toward the ideal converter:
+    relative L2 against exact attention falls monotonically with the density,
+    the direction of the paper's density sweep (Table b300-tuning), and the full
+    density reaches the ideal converter's error."""
+    (q, k, v), ops, s = gaussian_head_d128
+    ref = exact.attention(q, k, v, s)
+    rels = []
+    for kx in directp.EX2_PAIRS:
+        res = directp.forward_rows(*ops, np.arange(1024), s, ex2_pairs=kx, want_codes=False)
+        rels.append(exact.error_metrics(res["O"], ref)[1])
+    assert all(a > b for a, b in zip(rels, rels[1:])), rels
+    ideal = directp.forward_rows(*ops, np.arange(1024), s, mode="exp2", want_codes=False)
+    assert abs(rels[-1] - exact.error_metrics(ideal["O"], ref)[1]) < 1e-4
+
+
+def test_ex2_block_argmax_gets_code_six(gaussian_head_d128):
+    """At the block maximum x >= log2 6, so 2**x >= 6 saturates to code 6 on a
+    selected key as it does under the affine map."""
+    _, ops, s = gaussian_head_d128
+    q6 = mxfp4.scaled_operand(*ops[0:2])[:64]
+    k6 = mxfp4.scaled_operand(*ops[2:4])
+    raw = directp.raw_scores(q6, k6)
+    _, _, kk = directp.block_exponents_and_codes(raw, s, 1.5, 1.2, ex2_pairs=16)
+    am = raw.reshape(64, -1, 32).argmax(axis=-1)
+    assert np.all(np.take_along_axis(kk.reshape(64, -1, 32), am[..., None], -1) == 7)
