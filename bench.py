@@ -27,6 +27,7 @@ MXFP4_PEAK_TFLOPS = 10100.0   # MI355X dense FP4/FP6 matrix peak
 BF16_PEAK_TFLOPS = 2500.0     # MI355X dense BF16 matrix peak
 HBM_PEAK_GBS = 8000.0
 SPEC_CLOCK_GHZ = 2.4          # the clock the spec peaks assume
+EX2_SWEEP = (1, 2, 4, 16)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_mxfp4_long_b1h32_n16384_d128_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_04105_amd", "csrc", f)
                   for f in ("fwd_mxfp4.hip", "gfx950.hpp", "launch.hpp")]
@@ -262,6 +263,11 @@ def main():
     fns = {"fp4": fp4_step}
     if not args.no_bf16:
         fns["bf16"] = bf16_step
+    # native-exponential mixing (k of the 16 pairs of each 32-key block): the
+    # `accurate` policy's quarter and the exp2-only route, same inputs
+    for kx in EX2_SWEEP:
+        fns[f"ex2_{kx}"] = (lambda kx=kx: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out,
+                                                           ex2_pairs=kx))
     med, _ = _time_windows(torch, fns, max(1, args.steps // 2), args.windows)
     qms, _ = _time_windows(torch, {"quant": quant_step}, 3, 3)
 
@@ -307,6 +313,9 @@ def main():
         "fp4_ms_median_interleaved": round(med["fp4"], 5),
         "bf16_ms_median_interleaved": None if "bf16" not in med else round(med["bf16"], 5),
         "quantize_qkv_ms": round(qms["quant"], 5),
+        "ex2_pairs_sweep": {str(kx): {"ms": round(med[f"ex2_{kx}"], 5),
+                                      "tflops": round(flops / (med[f"ex2_{kx}"] * 1e-3) / 1e12, 2),
+                                      "vs_affine": round(med["fp4"] / med[f"ex2_{kx}"], 3)} for kx in EX2_SWEEP},
         "wall_ms_timed_region": round(wall_ms, 3),
         "roofline": roof,
         "gpu": torch.cuda.get_device_name(dev),

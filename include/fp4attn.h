@@ -108,6 +108,46 @@ fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_sc
                                      void* out, int out_dtype, void* stream);
 
 /*
+ * Options of the extended forward.  Fill with fp4attn_forward_options_init()
+ * and then change fields; struct_size must equal sizeof(fp4attn_forward_options)
+ * of the header the caller was built with.
+ *
+ *   affine_a, affine_b  the affine code map (init 1.5 / 1.2, the `fast` fit).
+ *   ex2_pairs           native-exponential mixing (Sec. "Fix 1": a selected
+ *                       pair may take the native exponential; Table
+ *                       policy-definition: the `accurate` policy does so on
+ *                       about a quarter of pair positions).  k in {0, 1, 2, 4,
+ *                       8, 16} of the 16 key pairs of every 32-key block (pair
+ *                       p = keys 2p, 2p+1, selected iff p % (16 / k) == 0) get
+ *                       the ideal code q = E2M1(2^x), x = y - E_B + log2 6
+ *                       evaluated as one fp32 fma, 2^x on the hardware
+ *                       exponential; the other pairs keep the affine map.
+ *                       init 0 (all affine); 16 is the exp2-only route.
+ */
+typedef struct fp4attn_forward_options {
+  uint32_t struct_size;
+  float affine_a;
+  float affine_b;
+  int32_t ex2_pairs;
+} fp4attn_forward_options;
+
+/* Writes the defaults listed above (and struct_size) into *opts; NULL is ignored. */
+void fp4attn_forward_options_init(fp4attn_forward_options* opts);
+
+/*
+ * fp4attn_forward_mxfp4 with options (NULL = the defaults).  Operands, layout
+ * and output as fp4attn_forward_mxfp4.  Errors: those of fp4attn_forward_mxfp4,
+ * plus INVALID_ARG for a struct_size other than sizeof(fp4attn_forward_options)
+ * or ex2_pairs outside {0, 1, 2, 4, 8, 16}.
+ */
+fp4attn_status fp4attn_forward_mxfp4_ex(const uint8_t* q_codes, const uint8_t* q_scales,
+                                        const uint8_t* k_codes, const uint8_t* k_scales,
+                                        const uint8_t* vt_codes, const uint8_t* vt_scales,
+                                        int64_t B, int64_t H, int64_t N, int64_t d,
+                                        float softmax_scale, const fp4attn_forward_options* opts,
+                                        void* out, int out_dtype, void* stream);
+
+/*
  * Same-design BF16 attention forward: the speed baseline of the paper's
  * canonical speedup t_BF16 / t_k (eq. canonical-speedup).  Textbook softmax
  * attention (eq. exact-attention) with the online recurrence
@@ -133,8 +173,9 @@ fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t ro
                                       void* dst, void* stream);
 
 /*
- * Test hook: runs exactly the forward kernel of fp4attn_forward_mxfp4 (same
- * launch configuration and arguments, writes `out` too) and additionally
+ * Test hook: runs exactly the forward kernel of fp4attn_forward_mxfp4_ex (same
+ * launch configuration and arguments, `opts` NULL = the defaults, writes `out`
+ * too) and additionally
  * dumps the Direct-P state of selected query rows (Alg. 2, steps 1-6):
  *
  *   row_ids    [n_rows] int64, flattened (b*H + h)*N + i, STRICTLY ASCENDING
@@ -154,14 +195,14 @@ fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t ro
  * may be NULL) and the launch is the plain forward kernel itself, so wg_clock
  * then records the clock of exactly the timed kernel.
  *
- * Errors: as fp4attn_forward_mxfp4, plus INVALID_ARG for n_rows < 0, a null
+ * Errors: as fp4attn_forward_mxfp4_ex, plus INVALID_ARG for n_rows < 0, a null
  * dump pointer when n_rows > 0, or a wg_clock that is not 16-byte aligned.
  */
 fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales,
                                            const uint8_t* k_codes, const uint8_t* k_scales,
                                            const uint8_t* vt_codes, const uint8_t* vt_scales,
                                            int64_t B, int64_t H, int64_t N, int64_t d,
-                                           float softmax_scale, float affine_a, float affine_b,
+                                           float softmax_scale, const fp4attn_forward_options* opts,
                                            void* out, int out_dtype,
                                            const int64_t* row_ids, int64_t n_rows,
                                            uint8_t* p_codes, int16_t* block_exp,

@@ -13,20 +13,29 @@ _i64 = ctypes.c_int64
 _int = ctypes.c_int
 _f32 = ctypes.c_float
 
-# name -> (argtypes); every entry point except the last three returns a status int
+
+class ForwardOptions(ctypes.Structure):
+    """fp4attn_forward_options (include/fp4attn.h)."""
+    _fields_ = [("struct_size", ctypes.c_uint32), ("affine_a", ctypes.c_float), ("affine_b", ctypes.c_float),
+                ("ex2_pairs", ctypes.c_int32)]
+
+
+# name -> argtypes; entry points not in RESTYPES return a status int
 SIGNATURES = {
     "fp4attn_quantize_mxfp4": [_c_p, _int, _i64, _i64, _i64, _int, _c_p, _c_p, _c_p],
     "fp4attn_forward_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32] * 3 + [_c_p, _int, _c_p],
     "fp4attn_forward_bf16": [_c_p] * 3 + [_i64] * 4 + [_f32, _c_p, _int, _c_p],
     "fp4attn_transpose_bf16": [_c_p, _i64, _i64, _i64, _c_p, _c_p],
-    "fp4attn_debug_directp_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32] * 3 + [_c_p, _int, _c_p, _i64]
-    + [_c_p] * 5 + [_c_p],
+    "fp4attn_forward_options_init": [ctypes.POINTER(ForwardOptions)],
+    "fp4attn_forward_mxfp4_ex": [_c_p] * 6 + [_i64] * 4 + [_f32, ctypes.POINTER(ForwardOptions), _c_p, _int, _c_p],
+    "fp4attn_debug_directp_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32, ctypes.POINTER(ForwardOptions)]
+    + [_c_p, _int, _c_p, _i64] + [_c_p] * 5 + [_c_p],
     "fp4attn_status_string": [_int],
     "fp4attn_last_error": [],
     "fp4attn_abi_version": [],
 }
 RESTYPES = {"fp4attn_status_string": ctypes.c_char_p, "fp4attn_last_error": ctypes.c_char_p,
-            "fp4attn_abi_version": ctypes.c_int}
+            "fp4attn_abi_version": ctypes.c_int, "fp4attn_forward_options_init": None}
 
 
 class Fp4AttnError(RuntimeError):
@@ -38,7 +47,7 @@ class Fp4AttnError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{LIB_PATH} is missing: build it with `python -m paper_2609_04105_amd.build` "
+            f"{LIB_PATH} is missing: build it with `python paper_2609_04105_amd/build.py` "
             "(or __graft_entry__.build()); there is no fallback path")
     handle = ctypes.CDLL(LIB_PATH)
     for name, args in SIGNATURES.items():

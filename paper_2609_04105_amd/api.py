@@ -9,7 +9,7 @@ import math
 
 import torch
 
-from ._lib import FP4ATTN_BF16, FP4ATTN_F32, check, lib
+from ._lib import FP4ATTN_BF16, FP4ATTN_F32, ForwardOptions, check, lib
 
 _DTYPES = {torch.float32: FP4ATTN_F32, torch.bfloat16: FP4ATTN_BF16}
 
@@ -91,21 +91,39 @@ def _out(out, B, H, N, d, out_dtype, device):
     return out
 
 
+def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0):
+    """An fp4attn_forward_options struct: the library's defaults, then the given fields."""
+    o = ForwardOptions()
+    lib.fp4attn_forward_options_init(ctypes.byref(o))
+    o.affine_a, o.affine_b, o.ex2_pairs = affine_a, affine_b, ex2_pairs
+    return o
+
+
 def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, softmax_scale=None,
-                  affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32):
-    """Direct-P full-MXFP4 attention forward; returns O [B, H, N, d]."""
+                  affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32, ex2_pairs=None):
+    """Direct-P full-MXFP4 attention forward; returns O [B, H, N, d].
+
+    ``ex2_pairs`` (0, 1, 2, 4, 8 or 16 of the 16 key pairs of each 32-key
+    block take the native exponential) selects the extended entry point; left
+    at None the plain forward runs.
+    """
     B, H, N, d = _fp4_shape(q_codes)
     ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
     _check_operands(B, H, N, d, ops)
     out = _out(out, B, H, N, d, out_dtype, q_codes.device)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    check(lib.fp4attn_forward_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
-                                    _DTYPES[out.dtype], _stream(out)))
+    if ex2_pairs is None:
+        check(lib.fp4attn_forward_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
+                                        _DTYPES[out.dtype], _stream(out)))
+    else:
+        o = forward_options(affine_a, affine_b, ex2_pairs)
+        check(lib.fp4attn_forward_mxfp4_ex(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
+                                           _DTYPES[out.dtype], _stream(out)))
     return out
 
 
 def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, row_ids, softmax_scale=None,
-                        affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False):
+                        affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False, ex2_pairs=0):
     """Forward plus the Direct-P state of the (strictly ascending) flattened ``row_ids``.
 
     Returns a dict: out, p_codes [R, N/2] uint8, block_exp [R, N/32] int16,
@@ -130,7 +148,8 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
     if wg_clock:
         res["wg_clock"] = torch.zeros((B * H * N // 128, 2), dtype=torch.int64, device=dev)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
+    o = forward_options(affine_a, affine_b, ex2_pairs)
+    check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
                                           _DTYPES[out_dtype], _ptr(row_ids) if R else None, R, _ptr(res["p_codes"]),
                                           _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),
                                           _ptr(res["wg_clock"]) if wg_clock else None, _stream(out)))

@@ -1,6 +1,6 @@
 """Build libfp4attn.so (the HIP kernels and the C-ABI) in-tree with hipcc for gfx950.
 
-Usage: python -m paper_2609_04105_amd.build [--jobs N]
+Usage: python paper_2609_04105_amd/build.py [--jobs N]   (does not import the package)
 """
 import argparse
 import os
@@ -14,10 +14,12 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libfp4attn.so")
-SOURCES = ["api.hip", "quantize.hip", "fwd_mxfp4.hip", "fwd_bf16.hip"]
+SOURCES = ["fwd_mxfp4.hip", "fwd_mxfp4_ex2.hip", "fwd_mxfp4_ex2_dense.hip", "fwd_bf16.hip", "api.hip",
+           "quantize.hip"]
 # The attention kernels never rely on NaN ordering in fmax; without this flag the
 # compiler canonicalizes every fmax operand with an extra v_max_f32.
-EXTRA = {"fwd_mxfp4.hip": ["-fno-honor-nans"], "fwd_bf16.hip": ["-fno-honor-nans"]}
+EXTRA = {f: ["-fno-honor-nans"] for f in ("fwd_mxfp4.hip", "fwd_mxfp4_ex2.hip", "fwd_mxfp4_ex2_dense.hip",
+                                          "fwd_bf16.hip")}
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -45,7 +47,7 @@ def _compile(src):
     return obj
 
 
-def build(jobs=4, verbose=True):
+def build(jobs=6, verbose=True):
     """Compile every HIP source for gfx950 and link the shared library (always rebuilds)."""
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=jobs) as ex:
@@ -63,5 +65,5 @@ def build(jobs=4, verbose=True):
 
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
-    ap.add_argument("--jobs", type=int, default=4)
+    ap.add_argument("--jobs", type=int, default=6)
     build(ap.parse_args().jobs)

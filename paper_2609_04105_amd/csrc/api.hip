@@ -70,6 +70,31 @@ fp4attn_status check_directp(const uint8_t* q_codes, const uint8_t* q_scales, co
   return check_attention_shape(B, H, N, d, softmax_scale, out_dtype);
 }
 
+fp4attn_forward_options default_options() {
+  fp4attn_forward_options o{};
+  o.struct_size = sizeof(fp4attn_forward_options);
+  o.affine_a = 1.5f;
+  o.affine_b = 1.2f;
+  o.ex2_pairs = 0;
+  return o;
+}
+
+// Options of the extended entry points: NULL means the defaults.
+fp4attn_status check_options(const fp4attn_forward_options* opts, fp4attn_forward_options* out) {
+  if (opts == nullptr) {
+    *out = default_options();
+    return FP4ATTN_OK;
+  }
+  if (opts->struct_size != sizeof(fp4attn_forward_options))
+    return fail(FP4ATTN_ERR_INVALID_ARG, "options struct_size %u, expected %zu", opts->struct_size,
+                sizeof(fp4attn_forward_options));
+  const int k = opts->ex2_pairs;
+  if (k != 0 && k != 1 && k != 2 && k != 4 && k != 8 && k != 16)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "ex2_pairs=%d is not one of 0, 1, 2, 4, 8, 16", k);
+  *out = *opts;
+  return FP4ATTN_OK;
+}
+
 fp4attn::DirectPArgs directp_args(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
                                   const uint8_t* k_scales, const uint8_t* vt_codes, const uint8_t* vt_scales,
                                   int64_t B, int64_t H, int64_t N, int64_t d, float softmax_scale, float affine_a,
@@ -130,15 +155,39 @@ fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_sc
   return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "forward launch");
 }
 
+void fp4attn_forward_options_init(fp4attn_forward_options* opts) {
+  if (opts != nullptr) *opts = default_options();
+}
+
+fp4attn_status fp4attn_forward_mxfp4_ex(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                                        const uint8_t* k_scales, const uint8_t* vt_codes, const uint8_t* vt_scales,
+                                        int64_t B, int64_t H, int64_t N, int64_t d, float softmax_scale,
+                                        const fp4attn_forward_options* opts, void* out, int out_dtype,
+                                        void* stream) {
+  fp4attn_forward_options o;
+  fp4attn_status st = check_options(opts, &o);
+  if (st != FP4ATTN_OK) return st;
+  st = check_directp(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d, softmax_scale,
+                     o.affine_a, o.affine_b, out, out_dtype);
+  if (st != FP4ATTN_OK) return st;
+  fp4attn::DirectPArgs a = directp_args(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
+                                        softmax_scale, o.affine_a, o.affine_b, out, out_dtype);
+  a.ex2_pairs = o.ex2_pairs;
+  return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "forward launch");
+}
+
 fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
                                            const uint8_t* k_scales, const uint8_t* vt_codes,
                                            const uint8_t* vt_scales, int64_t B, int64_t H, int64_t N, int64_t d,
-                                           float softmax_scale, float affine_a, float affine_b, void* out,
+                                           float softmax_scale, const fp4attn_forward_options* opts, void* out,
                                            int out_dtype, const int64_t* row_ids, int64_t n_rows, uint8_t* p_codes,
                                            int16_t* block_exp, int32_t* row_m, float* row_d, uint64_t* wg_clock,
                                            void* stream) {
-  const fp4attn_status st = check_directp(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
-                                          softmax_scale, affine_a, affine_b, out, out_dtype);
+  fp4attn_forward_options o;
+  fp4attn_status st = check_options(opts, &o);
+  if (st != FP4ATTN_OK) return st;
+  st = check_directp(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d, softmax_scale,
+                     o.affine_a, o.affine_b, out, out_dtype);
   if (st != FP4ATTN_OK) return st;
   if (n_rows < 0 || n_rows > 0x7fffffff) return fail(FP4ATTN_ERR_INVALID_ARG, "n_rows must be in [0, 2^31)");
   if (n_rows > 0) {
@@ -148,16 +197,17 @@ fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t
     REQUIRE_PTR(row_m);
     REQUIRE_PTR(row_d);
   }
+  if (wg_clock != nullptr && (reinterpret_cast<uintptr_t>(wg_clock) & 15) != 0)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "wg_clock is not 16-byte aligned");
   fp4attn::DirectPArgs a = directp_args(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
-                                        softmax_scale, affine_a, affine_b, out, out_dtype);
+                                        softmax_scale, o.affine_a, o.affine_b, out, out_dtype);
+  a.ex2_pairs = o.ex2_pairs;
   a.row_ids = n_rows > 0 ? row_ids : nullptr;
   a.n_rows = (int)n_rows;
   a.p_codes = p_codes;
   a.block_exp = block_exp;
   a.row_m = row_m;
   a.row_d = row_d;
-  if (wg_clock != nullptr && (reinterpret_cast<uintptr_t>(wg_clock) & 15) != 0)
-    return fail(FP4ATTN_ERR_INVALID_ARG, "wg_clock is not 16-byte aligned");
   a.wg_clock = reinterpret_cast<unsigned long long*>(wg_clock);
   return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "debug forward launch");
 }
@@ -208,6 +258,6 @@ const char* fp4attn_status_string(int status) {
 
 const char* fp4attn_last_error(void) { return g_last_error; }
 
-int fp4attn_abi_version(void) { return (1 << 16) | 1; }
+int fp4attn_abi_version(void) { return (1 << 16) | 2; }
 
 }  // extern "C"

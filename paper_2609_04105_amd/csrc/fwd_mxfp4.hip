@@ -1,471 +1,44 @@
-// Direct-P full-MXFP4 attention forward for gfx950.
-//
-// Method (paper Sec. "Direct-P", Alg. 2, eqs. affine-code-map,
-// represented-contributions, represented-output):
-//   raw   = block-scaled FP4 product of Q and K          (= 36 Qhat Khat^T)
-//   E_B   = floor(max_{j in B} raw_ij * c_y)              c_y = s log2(e) / 36
-//   q_ij  = E2M1(max(0, fma(c_a, raw_ij, k0 - A E_B)))     c_a = A c_y, k0 = A log2 6 + B
-//   O_i   = sum_B 2^(E_B - M_i) sum_j q_ij (6 Vhat_j) / (6 sum_B 2^(E_B - M_i) c_B)
-//
-// gfx950 design
-// - One workgroup = NW waves = 32 * NW query rows of one (batch, head); each
-//   wave owns 32 queries for the whole key loop.  Both products run on the
-//   scaled FP4 matrix unit (v_mfma_scale_f32_32x32x64_f8f6f4) in transposed
-//   form: S^T = K Q^T and O^T = V^T P^T.  Lane l then holds query l % 32 in
-//   every accumulator, so the per-row online state (integer reference M_i, the
-//   lazy power-of-two rescale) is a per-lane scalar and needs no cross-lane
-//   broadcast.
-// - Keys are fed to the S^T product in a permuted order (key_of_row below)
-//   so that, with the 32x32 accumulator layout, lane half h holds all 32
-//   scores of N32 block h of each 64-key step, in key order, in the registers
-//   of two QK subtiles.  Block maximum, block exponent and E2M1 codes are then
-//   lane-local, and the converted codes already form the lane's K64 P^T operand
-//   of the PV product (the paper's two N32 fragments published as one K64
-//   operand) with no cross-lane data movement.
-// - Code map: one v_fma_f32 with the clamp modifier per score on u / 8 (the
-//   median with 0 and 1 folds into it), then v_cvt_scalef32_pk_fp4_f32 with
-//   scale 1/8 (two scores per instruction); the clamp realises max(0, u) and
-//   saturation, and scaling by a power of two changes no rounding decision.
-// - Denominator c_B: an extra 16x16x128 product of the same P^T register with a
-//   constant indicator operand, so it uses exactly the codes and E8M0 bytes of
-//   PV and costs no vector-ALU work.
-// - K/V tiles of 128 keys are staged in LDS in matrix-operand order (each
-//   lane's 16-byte fragment contiguous): a ring of four tiles, filled from
-//   registers that fetch two or three tiles ahead.  The key loop is software
-//   pipelined two deep: while the vector ALU maps step g+1 to codes, the
-//   matrix unit runs PV of step g and QK of step g+2.
-// - Workgroups are remapped so that the query tiles of one head run on one XCD
-//   and share its L2 copy of that head's K/V.
-#include "gfx950.hpp"
-#include "launch.hpp"
+// Direct-P full-MXFP4 attention forward: host dispatch (the kernel and its
+// design are in fwd_mxfp4.hpp).  The EX2 = 0 variants are compiled here; the
+// native-exponential densities come from fwd_mxfp4_ex2*.hip, compiled in
+// parallel with this file.
+#include "fwd_mxfp4.hpp"
 
 namespace fp4attn {
+namespace directp_detail {
+
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 0)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 1)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 2)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 8)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16)
 
 namespace {
 
-constexpr int kBN = 128;   // keys per LDS tile
-constexpr int kTau = 8;    // lazy rescale: the reference may lag the row maximum by up to 8 binades
-constexpr int kStages = 4; // LDS ring depth in tiles
-constexpr double kLog2E = 1.4426950408889634;
-constexpr double kLog2Of6 = 2.584962500721156;
-
-struct KParams {
-  const uint8_t* qc;
-  const uint8_t* qs;
-  const uint8_t* kc;
-  const uint8_t* ks;
-  const uint8_t* vc;
-  const uint8_t* vs;
-  void* out;
-  int N, n_qtiles, total;
-  float c_y, c_a8, k0_8, a8;
-  const int64_t* row_ids;
-  int n_rows;
-  uint8_t* p_codes;
-  int16_t* block_exp;
-  int32_t* row_m;
-  float* row_d;
-  unsigned long long* wg_clock;
-};
-
-template <int D>
-struct Layout {
-  static constexpr int kCodes = (kBN / 32) * (D / 64) * 1024;  // K fragments [sub][chunk][lane][16 B]
-  static constexpr int kScales = (kBN / 32) * 64 * 4;          // [sub][lane] u32
-  static constexpr int vCodes = (kBN / 64) * (D / 32) * 1024;  // V^T fragments [step][chunk][lane][16 B]
-  static constexpr int vScales = (D / 32) * 64 * 4;            // [chunk][lane] u32
-  static constexpr int kOff = 0;
-  static constexpr int ksOff = kOff + kCodes;
-  static constexpr int vOff = ksOff + kScales;
-  static constexpr int vsOff = vOff + vCodes;
-  static constexpr int stage = vsOff + vScales;
-};
-
-// Key order of the S^T product.  Operand row m = 8 g + 4 h + i of QK subtile
-// `sub` (two subtiles per 64-key step) holds key 32 h + 16 (sub & 1) + 4 g + i of
-// step sub / 2.  With the 32x32 accumulator layout, lane half h then holds all
-// 32 keys of block h of the step, in key order, in the two subtiles' registers.
-__device__ __forceinline__ int key_of_row(int sub, int m) {
-  return 64 * (sub >> 1) + 32 * ((m >> 2) & 1) + 16 * (sub & 1) + 4 * (m >> 3) + (m & 3);
-}
-// Inverse: (subtile, operand row) of key k of a 128-key tile.
-__device__ __forceinline__ int sub_of_key(int k) { return 2 * (k >> 6) + ((k >> 4) & 1); }
-__device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * ((k >> 5) & 1) + (k & 3); }
-
-template <int D, int NW>
-struct TileRegs;
-
-// Placeholder for an unused staging set.
-template <int D>
-struct TileRegs<D, 0> {
-  __device__ __forceinline__ void load(const uint8_t*, const uint8_t*, const uint8_t*, const uint8_t*, int, int, int) {}
-  __device__ __forceinline__ void store(uint8_t*, int) const {}
-};
-
-template <int D, int NW>
-struct TileRegs {
-  static constexpr int NT = NW * 64;
-  static constexpr int nK = Layout<D>::kCodes / 16;
-  static constexpr int nV = Layout<D>::vCodes / 16;
-  static constexpr int KPT = (nK + NT - 1) / NT;
-  static constexpr int VPT = (nV + NT - 1) / NT;
-  v4i k[KPT];
-  v4i v[VPT];
-  unsigned ks, vs;
-
-  __device__ __forceinline__ void load(const uint8_t* kc, const uint8_t* ks_, const uint8_t* vc, const uint8_t* vs_,
-                                       int N, int key0, int tid) {
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nK % NT == 0 || slot < nK) {
-        const int m = slot & 63, rest = slot >> 6;
-        const int c = rest % (D / 64), sub = rest / (D / 64);
-        const int key = key_of_row(sub, m & 31);
-        const int j = 2 * c + (m >> 5);
-        k[i] = *reinterpret_cast<const v4i*>(kc + (size_t)(key0 + key) * (D / 2) + j * 16);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nV % NT == 0 || slot < nV) {
-        const int m = slot & 63, rest = slot >> 6;
-        const int cc = rest % (D / 32), s = rest / (D / 32);
-        const int row = cc * 32 + (m & 31);
-        v[i] = *reinterpret_cast<const v4i*>(vc + (size_t)row * (N / 2) + key0 / 2 + s * 32 + (m >> 5) * 16);
-      }
-    }
-    if (tid < kBN) {
-      const uint8_t* p = ks_ + (size_t)(key0 + tid) * (D / 32);
-      ks = D == 128 ? *reinterpret_cast<const uint32_t*>(p) : (unsigned)*reinterpret_cast<const uint16_t*>(p);
-    } else if (tid < kBN + D) {
-      const int row = tid - kBN;
-      vs = *reinterpret_cast<const uint32_t*>(vs_ + (size_t)row * (N / 32) + key0 / 32);
-    }
-  }
-
-  __device__ __forceinline__ void store(uint8_t* st, int tid) const {
-    using L = Layout<D>;
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nK % NT == 0 || slot < nK) *reinterpret_cast<v4i*>(st + L::kOff + slot * 16) = k[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nV % NT == 0 || slot < nV) *reinterpret_cast<v4i*>(st + L::vOff + slot * 16) = v[i];
-    }
-    if (tid < kBN) {
-      const int sub = sub_of_key(tid), m0 = row_of_key(tid);
-      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::ksOff) + sub * 64;
-      dst[m0] = ks;            // lanes 0..31 use scale bytes 0, 2 (d blocks 0, 2)
-      dst[m0 + 32] = ks >> 8;  // lanes 32..63 use bytes 1, 3
-    } else if (tid < kBN + D) {
-      const int row = tid - kBN, cc = row >> 5, m0 = row & 31;
-      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::vsOff) + cc * 64;
-      dst[m0] = vs;
-      dst[m0 + 32] = vs >> 8;
-    }
-  }
-};
-
-template <int D, int NW, bool DUMP, bool OUT_BF16>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_mxfp4_kernel(const KParams p) {
-  using L = Layout<D>;
-  constexpr int BM = NW * 32;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * L::stage];
-
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, lr = lane & 31;
-  const unsigned long long clk0 = __builtin_amdgcn_s_memtime(), rt0 = __builtin_amdgcn_s_memrealtime();
-  const int lin = xcd_remap(blockIdx.x, p.total);
-  const int bh = lin / p.n_qtiles, qt = lin % p.n_qtiles;
-  const int N = p.N;
-  const int qrow = qt * BM + wave * 32 + lr;
-
-  const uint8_t* kc = p.kc + (size_t)bh * N * (D / 2);
-  const uint8_t* ks = p.ks + (size_t)bh * N * (D / 32);
-  const uint8_t* vc = p.vc + (size_t)bh * D * (N / 2);
-  const uint8_t* vs = p.vs + (size_t)bh * D * (N / 32);
-
-  // Q^T operand, resident for the whole key loop.
-  v4i qf[D / 64];
-  {
-    const uint8_t* qrow_codes = p.qc + ((size_t)bh * N + qrow) * (D / 2);
-#pragma unroll
-    for (int c = 0; c < D / 64; ++c) qf[c] = *reinterpret_cast<const v4i*>(qrow_codes + (2 * c + h) * 16);
-  }
-  int qsc;
-  {
-    const uint8_t* qs = p.qs + ((size_t)bh * N + qrow) * (D / 32);
-    const unsigned raw = D == 128 ? *reinterpret_cast<const uint32_t*>(qs) : *reinterpret_cast<const uint16_t*>(qs);
-    qsc = (int)(raw >> (8 * h));
-  }
-
-  int slot = -1;
-  if constexpr (DUMP) {
-    const int64_t g = (int64_t)bh * N + qrow;
-    int lo = 0, hi = p.n_rows - 1;
-    while (lo <= hi) {
-      const int mid = (lo + hi) >> 1;
-      const int64_t v = p.row_ids[mid];
-      if (v == g) {
-        slot = mid;
-        break;
-      }
-      if (v < g) lo = mid + 1;
-      else hi = mid - 1;
-    }
-  }
-
-  // Denominator operand.  Read as the B operand of a 16x16x128 product, the K64
-  // P^T register of lane l is column l % 16 and K-block l / 16, i.e. query
-  // (l % 32)'s keys 32 (l / 32) .. +31.  Row 0 of this indicator matrix selects
-  // K-blocks 0 and 2 (query c's 64 keys), row 1 K-blocks 1 and 3 (query c + 16),
-  // so one 16x16x128 product yields every query's code sum with the P scales.
-  const int ones_word = (lane == 0 || lane == 32 || lane == 17 || lane == 49) ? 0x22222222 : 0;  // E2M1 1.0
-  const v4i ones = {ones_word, ones_word, ones_word, ones_word};
-
-  v16f O[D / 32];
-#pragma unroll
-  for (int c = 0; c < D / 32; ++c) O[c] = v16f{};
-  v4f Dacc = v4f{};  // lane c < 16: register 0 = query c, register 1 = query c + 16
-  float Mref = -1.0e6f;  // integer row reference (exact in fp32); no block seen yet
-
-  const int ntiles = N / kBN;
-  const int nsteps = 2 * ntiles;  // 64-key steps
-
-  // S^T of 64-key step `sl` (0 or 1) of the tile held in `st`: two 32-key blocks.
-  auto qk = [&](const uint8_t* st, auto SL_, v16f(&acc)[2]) {
-    constexpr int sl = decltype(SL_)::value;
-    static_for<2>([&](auto T_) {
-      constexpr int t = decltype(T_)::value;
-      constexpr int sub = 2 * sl + t;
-      v16f a = v16f{};
-      const int ksc = reinterpret_cast<const int*>(st + L::ksOff)[sub * 64 + lane];
-      static_for<D / 64>([&](auto C_) {
-        constexpr int c = decltype(C_)::value;
-        const v4i kf = *reinterpret_cast<const v4i*>(st + L::kOff + ((sub * (D / 64) + c) * 64 + lane) * 16);
-        a = mfma_fp4_32x32x64<2 * c, 2 * c>(kf, qf[c], a, ksc, qsc);
-      });
-      acc[t] = a;
-    });
-  };
-
-  // PV of step `s` (0 or 1) of the tile held in `st`, and the represented
-  // denominator from the same P^T operand and E8M0 bytes.
-  auto pv = [&](const uint8_t* st, auto S_, const v4i& P, int u) {
-    constexpr int s = decltype(S_)::value;
-    static_for<D / 32>([&](auto C_) {
-      constexpr int c = decltype(C_)::value;
-      const v4i vf = *reinterpret_cast<const v4i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 16);
-      const int vsc = reinterpret_cast<const int*>(st + L::vsOff)[c * 64 + lane];
-      O[c] = mfma_fp4_32x32x64<2 * s, 0>(vf, P, O[c], vsc, u);
-    });
-    Dacc = mfma_fp4_16x16x128<0, 0>(ones, P, Dacc, 127, u);
-  };
-
-  // Instruction order of one steady-state step (the region before the rescale
-  // branch): the step's LDS operand reads first, the block-maximum chain while
-  // they land, then every MFMA followed by a slice of the code map.
-  auto schedule_step = [&]() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);  // DS reads: V, K fragments and scales
-    __builtin_amdgcn_sched_group_barrier(0x002, 18, 0);  // VALU: block maximum, exponent, offset
-    static_for<D / 32 + 1 + 2 * (D / 64)>([&](auto) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // six VALU of the code map
-    });
-  };
-
-  // Direct-P for global 64-key step g (Alg. 2, steps 1-6).  Lane half h holds
-  // the 32 scores of block h of the step for query l % 32 (acc[0]: keys 0-15,
-  // acc[1]: keys 16-31), so the block maximum, the block exponent and the codes
-  // are all lane-local, and the codes land in the K64 P^T operand as they are
-  // converted.  Only the rare rescale branch exchanges the two halves' exponents.
-  auto directp = [&](const v16f(&acc)[2], int g, v4i& P, int& u, auto SCHED_) {
-    // 32 values in 16 three-input maxima (v_max3_f32)
-    float m = fmaxf(fmaxf(acc[0][0], acc[0][1]), acc[0][2]);
-#pragma unroll
-    for (int r = 3; r < 15; r += 2) m = fmaxf(fmaxf(m, acc[0][r]), acc[0][r + 1]);
-    m = fmaxf(fmaxf(m, acc[0][15]), acc[1][0]);
-#pragma unroll
-    for (int r = 1; r < 15; r += 2) m = fmaxf(fmaxf(m, acc[1][r]), acc[1][r + 1]);
-    m = fmaxf(m, acc[1][15]);
-    const float E = floorf(m * p.c_y);          // block exponent (Alg. 2, step 2)
-    const float c0 = fmaf(-p.a8, E, p.k0_8);    // (A (log2 6 - E) + B) / 8
-    // Code map on u / 8.  Every byte of the four words is written below; the
-    // first convert of each word takes its own input as the overwritten value.
-    unsigned w[4];
-    static_for<4>([&](auto I_) {
-      constexpr int i = decltype(I_)::value;
-      static_for<4>([&](auto W_) {
-        constexpr int wd = decltype(W_)::value;  // word wd holds keys 8 wd .. 8 wd + 7
-        const float lo = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[wd / 2][8 * (wd % 2) + 2 * i], c0), 0.0f, 1.0f);
-        const float hi = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, acc[wd / 2][8 * (wd % 2) + 2 * i + 1], c0), 0.0f, 1.0f);
-        w[wd] = cvt_pk_fp4<i>(i == 0 ? as_uint(lo) : w[wd], lo, hi, 0.125f);
-      });
-    });
-    P = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-    // Keep the code map in this basic block, next to the step's matrix work,
-    // instead of letting it sink below the rescale branch (emits nothing).
-    asm volatile("" ::"v"(P));
-    if constexpr (decltype(SCHED_)::value) schedule_step();
-    // Online integer reference with a lazy, exact power-of-two rescale of what
-    // PV has accumulated so far; the halves agree on the reference because the
-    // branch is taken by the whole wave and uses both halves' exponents.
-    if (__builtin_amdgcn_ballot_w64(E > Mref + kTau)) {
-      unsigned ea = as_uint(E), eb = ea;
-      swap_halves(ea, eb);  // each lane: (block-0 exponent, block-1 exponent)
-      const float Emax = fmaxf(as_float(ea), as_float(eb));
-      const float Mn = Emax > Mref + kTau ? Emax : Mref;
-      const int sh = (int)(Mref - Mn);
-#pragma unroll
-      for (int c = 0; c < D / 32; ++c)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
-      Dacc[0] = ldexpf(Dacc[0], sh);
-      Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
-      Mref = Mn;
-    }
-    // E8M0 byte of this lane's block: clamp(E - M + 127, 0, 254) (E - M <= kTau).
-    u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mref + 127.0f, 0, 0u);
-    if constexpr (DUMP) {
-      if (slot >= 0) {
-        const int kb = 2 * g + h;
-        *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
-        p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)(int)E;
-      }
-    }
-  };
-
-  // Pipeline.  LDS holds a ring of kStages = 4 tiles; at the start of tile t the
-  // staged registers of tile t+1 are published and tile t+3 is fetched into the
-  // freed register set (two sets: even and odd tiles).  In 64-key step g the
-  // matrix unit runs PV of step g and QK of step g+2 while the vector ALU runs
-  // Direct-P of step g+1.  Steps are unrolled eight at a time (four tiles), so
-  // every LDS offset and register set is a compile-time constant.
-  // With four waves each thread stages twice the bytes, so only one set is kept
-  // and tiles are fetched two (not three) tiles ahead.
-  constexpr bool kTwoSets = NW == 8;
-  constexpr int kAhead = kTwoSets ? 3 : 2;
-  TileRegs<D, NW> st_even;
-  TileRegs<D, kTwoSets ? NW : 0> st_odd;
-  st_even.load(kc, ks, vc, vs, N, 0, tid);
-  st_even.store(lds, tid);
-  if constexpr (kTwoSets) {
-    if (ntiles > 1) st_odd.load(kc, ks, vc, vs, N, kBN, tid);
-    if (ntiles > 2) st_even.load(kc, ks, vc, vs, N, 2 * kBN, tid);
-  } else {
-    if (ntiles > 1) st_even.load(kc, ks, vc, vs, N, kBN, tid);
-  }
-  __syncthreads();
-
-  // Two S^T buffers and two P operands alternate with the step parity.
-  v16f SA[2], SB[2];
-  v4i PA, PB;
-  int uA, uB;
-  qk(lds, std::integral_constant<int, 0>{}, SA);
-  directp(SA, 0, PA, uA, std::false_type{});
-  qk(lds, std::integral_constant<int, 1>{}, SA);
-
-  // One step of the pipeline; j is the step's position in its group of eight.
-  // GUARD: the tail group, where QK, Direct-P or the step itself may not exist.
-  auto step = [&](auto J_, auto GUARD_, int g) {
-    constexpr int j = decltype(J_)::value;
-    constexpr bool guard = decltype(GUARD_)::value;
-    constexpr int sl = j % 2;                 // step within its tile
-    constexpr int b_cur = (j / 2) % kStages;  // ring slot of tile t
-    constexpr int b_nxt = (j / 2 + 1) % kStages;
-    auto& S_in = (sl == 0) ? SA : SB;   // S^T of step g+1
-    auto& S_out = (sl == 0) ? SB : SA;  // S^T of step g+2
-    auto& P_cur = (sl == 0) ? PA : PB;  // P of step g
-    auto& u_cur = (sl == 0) ? uA : uB;
-    auto& P_nxt = (sl == 0) ? PB : PA;  // P of step g+1
-    auto& u_nxt = (sl == 0) ? uB : uA;
-    const int t = g >> 1;
-    if constexpr (sl == 0) {
-      auto publish = [&](auto& set) {  // `set` holds tile t+1
-        if (!guard || t + 1 < ntiles) set.store(lds + b_nxt * L::stage, tid);
-        __syncthreads();
-        if (t + kAhead < ntiles) set.load(kc, ks, vc, vs, N, (t + kAhead) * kBN, tid);
-      };
-      if constexpr (kTwoSets && (j / 2) % 2 == 0) publish(st_odd);
-      else publish(st_even);
-    }
-    pv(lds + b_cur * L::stage, std::integral_constant<int, sl>{}, P_cur, u_cur);
-    if (!guard || g + 2 < nsteps) {
-      qk(lds + b_nxt * L::stage, std::integral_constant<int, sl>{}, S_out);
-      // Issue QK of step g+2 in this step (it would otherwise sink next to its
-      // consumer in step g+1 and serialise with the code map); emits nothing.
-      asm volatile("" ::"v"(S_out[0]), "v"(S_out[1]));
-    }
-    if (!guard || g + 1 < nsteps) directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
-  };
-
-
-  int g0 = 0;
-  for (; g0 + 8 <= nsteps - 2; g0 += 8) {
-    static_for<8>([&](auto J_) { step(J_, std::false_type{}, g0 + decltype(J_)::value); });
-  }
-  // tail: at most nine steps remain (nsteps - 2 - g0 < 8)
-  static_for<10>([&](auto J_) {
-    const int g = g0 + decltype(J_)::value;
-    if (g < nsteps) step(J_, std::true_type{}, g);
-  });
-
-  // Epilogue: O = acc / (6 D).  The denominator sits in register 0 of the lower half.
-  const float d_lo = lane_read(Dacc[0], lane & 15), d_hi = lane_read(Dacc[1], lane & 15);
-  const float Dfin = (lane & 16) ? d_hi : d_lo;  // query lane % 32
-  const float inv = 1.0f / (6.0f * Dfin);
-  const size_t orow = ((size_t)bh * N + qrow) * D;
-#pragma unroll
-  for (int c = 0; c < D / 32; ++c) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int col = 32 * c + 8 * g + 4 * h;
-      const float o0 = O[c][4 * g] * inv, o1 = O[c][4 * g + 1] * inv;
-      const float o2 = O[c][4 * g + 2] * inv, o3 = O[c][4 * g + 3] * inv;
-      if constexpr (OUT_BF16) {
-        typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
-        const unsigned w0 = __builtin_bit_cast(unsigned, bf2{(__bf16)o0, (__bf16)o1});
-        const unsigned w1 = __builtin_bit_cast(unsigned, bf2{(__bf16)o2, (__bf16)o3});
-        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.out) + orow + col) = uint2{w0, w1};
-      } else {
-        *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.out) + orow + col) = float4{o0, o1, o2, o3};
-      }
-    }
-  }
-  if constexpr (DUMP) {
-    if (slot >= 0 && h == 0) {
-      p.row_m[slot] = (int)Mref;
-      p.row_d[slot] = Dfin;
-    }
-  }
-  if (p.wg_clock != nullptr && tid == 0) {
-    // shader-clock cycles and 100 MHz constant-clock ticks this workgroup was resident
-    const unsigned long long clk1 = __builtin_amdgcn_s_memtime(), rt1 = __builtin_amdgcn_s_memrealtime();
-    p.wg_clock[2 * blockIdx.x] = clk1 - clk0;
-    p.wg_clock[2 * blockIdx.x + 1] = rt1 - rt0;
+template <int D, int NW, bool DUMP>
+hipError_t dispatch_ex2(const KParams& kp, int ex2, hipStream_t stream) {
+  switch (ex2) {
+    case 0: return launch_directp<D, NW, DUMP, 0>(kp, stream);
+    case 1: return launch_directp<D, NW, DUMP, 1>(kp, stream);
+    case 2: return launch_directp<D, NW, DUMP, 2>(kp, stream);
+    case 4: return launch_directp<D, NW, DUMP, 4>(kp, stream);
+    case 8: return launch_directp<D, NW, DUMP, 8>(kp, stream);
+    case 16: return launch_directp<D, NW, DUMP, 16>(kp, stream);
+    default: return hipErrorInvalidValue;
   }
 }
 
-template <int D, int NW, bool DUMP, bool OUT_BF16>
-hipError_t launch_variant(const KParams& kp, hipStream_t stream) {
-  hipLaunchKernelGGL((fwd_mxfp4_kernel<D, NW, DUMP, OUT_BF16>), dim3(kp.total), dim3(NW * 64), 0, stream, kp);
-  return hipGetLastError();
-}
-
 template <int D, int NW>
-hipError_t dispatch_flags(const KParams& kp, bool dump, bool out_bf16, hipStream_t stream) {
-  if (dump) return out_bf16 ? launch_variant<D, NW, true, true>(kp, stream) : launch_variant<D, NW, true, false>(kp, stream);
-  return out_bf16 ? launch_variant<D, NW, false, true>(kp, stream) : launch_variant<D, NW, false, false>(kp, stream);
+hipError_t dispatch_dump(const KParams& kp, bool dump, int ex2, hipStream_t stream) {
+  return dump ? dispatch_ex2<D, NW, true>(kp, ex2, stream) : dispatch_ex2<D, NW, false>(kp, ex2, stream);
 }
 
 }  // namespace
+}  // namespace directp_detail
 
 hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
+  using namespace directp_detail;
   KParams kp{};
   kp.qc = a.q_codes;
   kp.qs = a.q_scales;
@@ -483,6 +56,8 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   kp.c_a8 = c_a * 0.125f;
   kp.k0_8 = k0 * 0.125f;
   kp.a8 = a.affine_a * 0.125f;
+  kp.k1 = (float)kLog2Of6;
+  kp.out_bf16 = a.out_bf16;
   kp.row_ids = a.row_ids;
   kp.n_rows = a.n_rows;
   kp.p_codes = a.p_codes;
@@ -497,9 +72,10 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   const int BM = wide ? 256 : 128;
   kp.n_qtiles = a.N / BM;
   kp.total = kp.n_qtiles * bh;
+  const int ex2 = a.ex2_pairs;
   if (a.d == 128)
-    return wide ? dispatch_flags<128, 8>(kp, dump, a.out_bf16, stream) : dispatch_flags<128, 4>(kp, dump, a.out_bf16, stream);
-  return wide ? dispatch_flags<64, 8>(kp, dump, a.out_bf16, stream) : dispatch_flags<64, 4>(kp, dump, a.out_bf16, stream);
+    return wide ? dispatch_dump<128, 8>(kp, dump, ex2, stream) : dispatch_dump<128, 4>(kp, dump, ex2, stream);
+  return wide ? dispatch_dump<64, 8>(kp, dump, ex2, stream) : dispatch_dump<64, 4>(kp, dump, ex2, stream);
 }
 
 }  // namespace fp4attn

@@ -25,6 +25,7 @@ struct DirectPArgs {
   int B, H, N, d;
   int out_bf16;
   float softmax_scale, affine_a, affine_b;
+  int ex2_pairs;  // pairs of 16 per 32-key block that take the native exponential
   // test hook (all null / zero for the plain forward)
   const int64_t* row_ids;
   int n_rows;

@@ -12,7 +12,7 @@ O_REL_L2_MAX = 2e-3        # output relative L2 error bound
 O_COS_MIN = 0.9999         # output cosine bound
 
 
-def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_codes=True):
+def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_codes=True, ex2_pairs=0):
     """Run the oracle on flattened query ``rows`` of fp64 arrays q, k, v [B, H, N, d].
 
     The oracle quantizes its own operands (oracle.mxfp4).  Returns a dict of
@@ -33,7 +33,7 @@ def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_c
         kc, ks = mxfp4.quantize(k[b, h], axis=-1)
         vc, vs = mxfp4.quantize(v[b, h], axis=-2)
         res = directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(local)), softmax_scale,
-                                   affine_a, affine_b, want_codes=want_codes)
+                                   affine_a, affine_b, want_codes=want_codes, ex2_pairs=ex2_pairs)
         for key in res:
             out[key][sel] = res[key]
     return out

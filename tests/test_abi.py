@@ -78,6 +78,27 @@ def test_quantize_and_bf16_validation(lib):
     t = lib.fp4attn_transpose_bf16
     assert t(FAKE[0], 1, 7, 8, FAKE[1], None) == 1
     d = lib.fp4attn_debug_directp_mxfp4
-    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, FAKE[7], -1, *FAKE[:4], None, None) == 1   # n_rows < 0
-    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 0, FAKE[7], 1, *FAKE[:4], ctypes.c_void_p(4096 + 8),
+    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, FAKE[7], -1, *FAKE[:4], None, None) == 1  # n_rows < 0
+    assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, FAKE[7], 1, *FAKE[:4], ctypes.c_void_p(4096 + 8),
              None) == 1                                                 # misaligned wg_clock
+
+
+def test_forward_options(lib):
+    from paper_2609_04105_amd import _lib
+    o = _lib.ForwardOptions()
+    assert ctypes.sizeof(o) == 16
+    lib.fp4attn_forward_options_init(ctypes.byref(o))
+    assert (o.struct_size, o.affine_a, o.ex2_pairs) == (16, 1.5, 0) and abs(o.affine_b - 1.2) < 1e-6
+    e = lib.fp4attn_forward_mxfp4_ex
+    for kx in (3, 5, 32, -1):
+        o.ex2_pairs = kx
+        assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
+    o.ex2_pairs = 4
+    o.struct_size = 12
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
+    o.struct_size = 16
+    o.affine_a = 0.0
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
+    o.affine_a = 1.5
+    assert e(*FAKE[:6], 1, 1, 128, 80, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 2     # d = 80
+    assert e(None, *FAKE[1:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, None) == 1

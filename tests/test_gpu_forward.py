@@ -21,19 +21,20 @@ def fa():
     return fa
 
 
-def _run_and_check(fa, host64, dev, rows, label, softmax_scale=None, affine=(1.5, 1.2)):
+def _run_and_check(fa, host64, dev, rows, label, softmax_scale=None, affine=(1.5, 1.2), ex2_pairs=None):
     q, k, v = host64
     B, H, N, d = q.shape
     s = 1.0 / np.sqrt(d) if softmax_scale is None else softmax_scale
     ops = gpu_operands(*dev)
     row_ids = torch.from_numpy(np.asarray(rows, dtype=np.int64)).cuda()
-    print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)}", flush=True)
-    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, affine_a=affine[0], affine_b=affine[1])
-    out = fa.forward_mxfp4(*ops, softmax_scale=s, affine_a=affine[0], affine_b=affine[1])
+    print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)} ex2_pairs={ex2_pairs}", flush=True)
+    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, affine_a=affine[0], affine_b=affine[1],
+                                  ex2_pairs=ex2_pairs or 0)
+    out = fa.forward_mxfp4(*ops, softmax_scale=s, affine_a=affine[0], affine_b=affine[1], ex2_pairs=ex2_pairs)
     torch.cuda.synchronize()
     # the test hook runs the same kernel: identical output
     assert torch.equal(out, dump["out"]), f"{label}: debug launch output differs from the forward"
-    ref = oracle_rows(q, k, v, rows, s, *affine)
+    ref = oracle_rows(q, k, v, rows, s, *affine, ex2_pairs=ex2_pairs or 0)
     mismatch = check_directp_dump(dump, ref, label)
     got = out.reshape(-1, d)[torch.from_numpy(np.asarray(rows)).cuda()].cpu().numpy()
     rel, cos = rel_l2_cos(got, ref["O"])
@@ -157,3 +158,59 @@ def test_workgroup_clock_record(fa, B, H, N, d, wgs, n_dump):
     ghz = float(c[:, 0].sum()) / (float(c[:, 1].sum()) / 100e6) / 1e9
     print(f"[clock] {ghz:.3f} GHz", flush=True)
     assert 0.3 < ghz < 3.0
+
+
+@pytest.mark.parametrize("ex2_pairs", [1, 2, 4, 8, 16])
+def test_ex2_mixing_small_all_rows(fa, ex2_pairs):
+    """Native-exponential pair mixing against the oracle's fp32 decision (the
+    hardware exponential may move a value across an E2M1 boundary only within
+    its last bits, inside the 1e-4 code-mismatch gate)."""
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    _run_and_check(fa, host64, dev, workloads.sampled_rows("small_b1h8_n1024_d64"), f"small ex2={ex2_pairs}",
+                   ex2_pairs=ex2_pairs)
+
+
+@pytest.mark.parametrize("ex2_pairs", [4, 16])
+def test_ex2_mixing_long_sampled_rows(fa, ex2_pairs):
+    name = "long_b1h32_n16384_d128"
+    host64, dev = load_workload(name)
+    _run_and_check(fa, host64, dev, workloads.sampled_rows(name), f"{name} ex2={ex2_pairs}", ex2_pairs=ex2_pairs)
+
+
+def test_extended_entry_with_defaults_is_the_plain_forward(fa):
+    host64, dev = load_workload("outlier_b2h16_n4096_d128")
+    ops = gpu_operands(*dev)
+    a = fa.forward_mxfp4(*ops)
+    b = fa.forward_mxfp4(*ops, ex2_pairs=0)
+    c = fa.forward_mxfp4(*ops, out_dtype=torch.bfloat16, ex2_pairs=0)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert torch.equal(c, a.to(torch.bfloat16))
+
+
+def test_ex2_density_fidelity_against_exact_attention(fa):
+    """Operator error of each density against exact attention on the unquantized
+    inputs (Sec. "Metrics": cosine, relative L2, RMSE), 4096 sampled rows of the
+    long workload: more native-exponential pairs, lower error, as in the paper's
+    density sweep (Table b300-tuning)."""
+    from oracle import exact
+    name = "long_b1h32_n16384_d128"
+    (q, k, v), dev = load_workload(name)
+    ops = gpu_operands(*dev)
+    rows = workloads.sampled_rows(name)
+    B, H, N, d = q.shape
+    s = 1.0 / np.sqrt(d)
+    ref = np.zeros((len(rows), d))
+    for bh in np.unique(rows // N):
+        sel = np.nonzero(rows // N == bh)[0]
+        b, h = divmod(int(bh), H)
+        ref[sel] = exact.attention(q[b, h][rows[sel] % N], k[b, h], v[b, h], s)
+    idx = torch.from_numpy(rows).cuda()
+    rels = []
+    for kx in (0, 1, 2, 4, 16):
+        out = fa.forward_mxfp4(*ops, ex2_pairs=kx)
+        got = out.reshape(-1, d)[idx].cpu().numpy()
+        cos, rel, rmse = exact.error_metrics(got, ref)
+        print(f"[fidelity] ex2_pairs={kx:2d} cos {cos:.6f} rel-L2 {rel:.6f} RMSE {rmse:.6f}", flush=True)
+        rels.append(rel)
+    assert all(a > b for a, b in zip(rels, rels[1:])), rels
