@@ -20,6 +20,8 @@ mxfp4    MXFP4 input quantizer: E2M1 codes + E8M0 amplitude per 32 values
 directp  Direct-P attention (Sec. "Direct-P", Fix 1 and Fix 2, Alg. 2,
          eqs. ideal-code-path, affine-code-map, represented-contributions,
          represented-output), brute-force and online (tiled) forms.
+guard    the sampled QK guard of Alg. 3 (Sec. "Fix 3"): anchor permutation,
+         margin M, stored-scale shift L and the floored working byte.
 exact    textbook softmax attention (eq. attention-intro / exact-attention)
          and the online-softmax recurrence (eq. online-recurrence).
 prange   the probability-format range diagnostic of Table p-range
