@@ -28,9 +28,10 @@ BF16_PEAK_TFLOPS = 2500.0     # MI355X dense BF16 matrix peak
 HBM_PEAK_GBS = 8000.0
 SPEC_CLOCK_GHZ = 2.4          # the clock the spec peaks assume
 EX2_SWEEP = (1, 2, 4, 16)
+GUARD_ML = (110, 16)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_mxfp4_long_b1h32_n16384_d128_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_04105_amd", "csrc", f)
-                  for f in ("fwd_mxfp4.hip", "gfx950.hpp", "launch.hpp")]
+                  for f in ("fwd_mxfp4.hpp", "fwd_mxfp4.hip", "gfx950.hpp", "launch.hpp")]
 
 
 def _source_sha():
@@ -268,6 +269,10 @@ def main():
     for kx in EX2_SWEEP:
         fns[f"ex2_{kx}"] = (lambda kx=kx: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out,
                                                            ex2_pairs=kx))
+    # the sampled QK guard (Alg. 3) on anchor-ordered K and V, the paper's (M, L) = (110, 16)
+    ops_anchored = fa.quantize_qkv(q, k, v, anchored=True)
+    fns["guard"] = lambda: fa.forward_mxfp4(*ops_anchored, softmax_scale=w.softmax_scale, out=out,
+                                            guard=GUARD_ML)
     med, _ = _time_windows(torch, fns, max(1, args.steps // 2), args.windows)
     qms, _ = _time_windows(torch, {"quant": quant_step}, 3, 3)
 
@@ -316,6 +321,8 @@ def main():
         "ex2_pairs_sweep": {str(kx): {"ms": round(med[f"ex2_{kx}"], 5),
                                       "tflops": round(flops / (med[f"ex2_{kx}"] * 1e-3) / 1e12, 2),
                                       "vs_affine": round(med["fp4"] / med[f"ex2_{kx}"], 3)} for kx in EX2_SWEEP},
+        "guard_110_16": {"ms": round(med["guard"], 5), "tflops": round(flops / (med["guard"] * 1e-3) / 1e12, 2),
+                         "vs_online": round(med["fp4"] / med["guard"], 3)},
         "wall_ms_timed_region": round(wall_ms, 3),
         "roofline": roof,
         "gpu": torch.cuda.get_device_name(dev),

@@ -75,6 +75,22 @@ fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t ba
                                       void* stream);
 
 /*
+ * fp4attn_quantize_mxfp4 of the rows put in anchor order first (Sec. "Fix 3":
+ * before the launch, globally distributed K/V rows move into the first key
+ * tile; exact attention does not change).  Row r of the quantized matrix is
+ * source row pi(r): for r < n_anchor, r * (rows / n_anchor) (evenly spread
+ * anchors); the remaining rows follow in their original order.  Used for K
+ * (axis 1) and V (axis 0, so V's 32-key blocks follow the new key order) of
+ * the guarded forward, with n_anchor = 128 (its first key tile).
+ *
+ * Errors: those of fp4attn_quantize_mxfp4, plus INVALID_ARG if n_anchor < 1 or
+ * n_anchor does not divide rows.
+ */
+fp4attn_status fp4attn_quantize_mxfp4_anchored(const void* src, int src_dtype, int64_t batch,
+                                               int64_t rows, int64_t cols, int axis, int64_t n_anchor,
+                                               uint8_t* codes, uint8_t* scales, void* stream);
+
+/*
  * Direct-P full-MXFP4 attention forward, noncausal (Sec. "Direct-P", Alg. 2,
  * eqs. affine-code-map, represented-contributions, represented-output).
  *
@@ -123,12 +139,32 @@ fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_sc
  *                       evaluated as one fp32 fma, 2^x on the hardware
  *                       exponential; the other pairs keep the affine map.
  *                       init 0 (all affine); 16 is the exp2-only route.
+ *   guard               1: the sampled QK guard of Alg. 3 replaces the online
+ *                       row reference.  The first 128 keys are the anchor set
+ *                       (K and V quantized with
+ *                       fp4attn_quantize_mxfp4_anchored, n_anchor = 128); per
+ *                       row, with y = raw * softmax_scale * log2(e) / 36 in
+ *                       fp32 and Y = the largest y over the anchors, the
+ *                       reference is R = fp32(Y + guard_margin), the block
+ *                       exponent e_B = floor(fp32(max_B y - R)), the working
+ *                       byte ubar_B = clamp(e_B + 127, guard_shift + 1, 254)
+ *                       (floored before the codes are formed), the codes
+ *                       those of Alg. 2 with x = y - T + log2 6,
+ *                       T = fp32(R + ubar_B - 127), and the published E8M0
+ *                       byte ubar_B - guard_shift.  init 0.  Built for
+ *                       ex2_pairs 0, 4 and 16.
+ *   guard_margin        M, guard_shift  L: integers >= 0 with M + L <= 126
+ *                       (Alg. 3 step 2); init 110 / 16, the paper's setting
+ *                       for its 1.3B video model.
  */
 typedef struct fp4attn_forward_options {
   uint32_t struct_size;
   float affine_a;
   float affine_b;
   int32_t ex2_pairs;
+  int32_t guard;
+  int32_t guard_margin;
+  int32_t guard_shift;
 } fp4attn_forward_options;
 
 /* Writes the defaults listed above (and struct_size) into *opts; NULL is ignored. */
@@ -137,8 +173,10 @@ void fp4attn_forward_options_init(fp4attn_forward_options* opts);
 /*
  * fp4attn_forward_mxfp4 with options (NULL = the defaults).  Operands, layout
  * and output as fp4attn_forward_mxfp4.  Errors: those of fp4attn_forward_mxfp4,
- * plus INVALID_ARG for a struct_size other than sizeof(fp4attn_forward_options)
- * or ex2_pairs outside {0, 1, 2, 4, 8, 16}.
+ * plus INVALID_ARG for a struct_size other than sizeof(fp4attn_forward_options),
+ * ex2_pairs outside {0, 1, 2, 4, 8, 16}, guard not 0 or 1, or a guard margin
+ * and shift outside the budget; UNSUPPORTED for the guard with ex2_pairs not
+ * in {0, 4, 16}.
  */
 fp4attn_status fp4attn_forward_mxfp4_ex(const uint8_t* q_codes, const uint8_t* q_scales,
                                         const uint8_t* k_codes, const uint8_t* k_scales,
@@ -182,8 +220,10 @@ fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t ro
  *              (rows not found by the kernel's binary search are not dumped)
  *   p_codes    [n_rows, N/2]  the P codes fed to the PV product, nibble-packed
  *   block_exp  [n_rows, N/32] int16 absolute block exponents E_B
- *   row_m      [n_rows] int32 final integer row reference M_i
- *   row_d      [n_rows] fp32 represented denominator relative to 2^M_i
+ *   row_m      [n_rows] int32 final integer row reference M_i (0 under the guard)
+ *   row_d      [n_rows] fp32 represented denominator relative to 2^M_i (under
+ *              the guard: sum_B 2^(u'_B - 127) c_B with the published bytes)
+ *              (block_exp holds the working exponents ubar_B - 127 under the guard)
  *   wg_clock   optional (NULL: not written), [B*H*N/128][2] uint64: workgroup
  *              w of the launch writes entry [w][0], the shader-clock cycles
  *              it was resident, and [w][1], the same interval in ticks of the

@@ -33,11 +33,12 @@ def _need(t, name, dtype=None, ndim=None):
         raise ValueError(f"{name} must have {ndim} dimensions, got shape {tuple(t.shape)}")
 
 
-def quantize_mxfp4(x, axis=-1):
+def quantize_mxfp4(x, axis=-1, n_anchor=0):
     """MXFP4 codes and E8M0 scales of ``x`` [..., rows, cols] (fp32 or bf16).
 
     axis=-1: blocks of 32 along cols -> codes [..., rows, cols/2], scales [..., rows, cols/32].
     axis=-2: blocks along rows, stored transposed -> codes [..., cols, rows/2], scales [..., cols, rows/32].
+    n_anchor > 0: the rows are taken in anchor order (fp4attn_quantize_mxfp4_anchored).
     """
     _need(x, "x", (torch.float32, torch.bfloat16))
     if x.dim() < 2:
@@ -53,16 +54,22 @@ def quantize_mxfp4(x, axis=-1):
         raise ValueError("axis must be -1 or -2")
     codes = torch.empty(cshape, dtype=torch.uint8, device=x.device)
     scales = torch.empty(sshape, dtype=torch.uint8, device=x.device)
-    check(lib.fp4attn_quantize_mxfp4(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, _ptr(codes),
-                                     _ptr(scales), _stream(x)))
+    if n_anchor:
+        check(lib.fp4attn_quantize_mxfp4_anchored(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, n_anchor,
+                                                  _ptr(codes), _ptr(scales), _stream(x)))
+    else:
+        check(lib.fp4attn_quantize_mxfp4(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, _ptr(codes),
+                                         _ptr(scales), _stream(x)))
     return codes, scales
 
 
-def quantize_qkv(q, k, v):
-    """MXFP4 operands of the forward: Q, K along d; V along the sequence (transposed)."""
+def quantize_qkv(q, k, v, anchored=False):
+    """MXFP4 operands of the forward: Q, K along d; V along the sequence (transposed).
+    ``anchored``: K and V in the anchor key order of the guarded forward (128 anchors)."""
+    n_anchor = 128 if anchored else 0
     qc, qs = quantize_mxfp4(q, axis=-1)
-    kc, ks = quantize_mxfp4(k, axis=-1)
-    vc, vs = quantize_mxfp4(v, axis=-2)
+    kc, ks = quantize_mxfp4(k, axis=-1, n_anchor=n_anchor)
+    vc, vs = quantize_mxfp4(v, axis=-2, n_anchor=n_anchor)
     return qc, qs, kc, ks, vc, vs
 
 
@@ -91,39 +98,44 @@ def _out(out, B, H, N, d, out_dtype, device):
     return out
 
 
-def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0):
-    """An fp4attn_forward_options struct: the library's defaults, then the given fields."""
+def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0, guard=None):
+    """An fp4attn_forward_options struct: the library's defaults, then the given
+    fields; ``guard`` = (margin, shift) turns the sampled guard on."""
     o = ForwardOptions()
     lib.fp4attn_forward_options_init(ctypes.byref(o))
     o.affine_a, o.affine_b, o.ex2_pairs = affine_a, affine_b, ex2_pairs
+    if guard is not None:
+        o.guard, (o.guard_margin, o.guard_shift) = 1, guard
     return o
 
 
 def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, softmax_scale=None,
-                  affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32, ex2_pairs=None):
+                  affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32, ex2_pairs=None, guard=None):
     """Direct-P full-MXFP4 attention forward; returns O [B, H, N, d].
 
     ``ex2_pairs`` (0, 1, 2, 4, 8 or 16 of the 16 key pairs of each 32-key
-    block take the native exponential) selects the extended entry point; left
-    at None the plain forward runs.
+    block take the native exponential) or ``guard`` = (margin, shift) (the
+    sampled guard; K and V from ``quantize_qkv(..., anchored=True)``) select the
+    extended entry point; with both None the plain forward runs.
     """
     B, H, N, d = _fp4_shape(q_codes)
     ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
     _check_operands(B, H, N, d, ops)
     out = _out(out, B, H, N, d, out_dtype, q_codes.device)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    if ex2_pairs is None:
+    if ex2_pairs is None and guard is None:
         check(lib.fp4attn_forward_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
                                         _DTYPES[out.dtype], _stream(out)))
     else:
-        o = forward_options(affine_a, affine_b, ex2_pairs)
+        o = forward_options(affine_a, affine_b, ex2_pairs or 0, guard)
         check(lib.fp4attn_forward_mxfp4_ex(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
                                            _DTYPES[out.dtype], _stream(out)))
     return out
 
 
 def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, row_ids, softmax_scale=None,
-                        affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False, ex2_pairs=0):
+                        affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False, ex2_pairs=0,
+                        guard=None):
     """Forward plus the Direct-P state of the (strictly ascending) flattened ``row_ids``.
 
     Returns a dict: out, p_codes [R, N/2] uint8, block_exp [R, N/32] int16,
@@ -148,7 +160,7 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
     if wg_clock:
         res["wg_clock"] = torch.zeros((B * H * N // 128, 2), dtype=torch.int64, device=dev)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    o = forward_options(affine_a, affine_b, ex2_pairs)
+    o = forward_options(affine_a, affine_b, ex2_pairs, guard)
     check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
                                           _DTYPES[out_dtype], _ptr(row_ids) if R else None, R, _ptr(res["p_codes"]),
                                           _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),

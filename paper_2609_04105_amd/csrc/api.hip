@@ -76,6 +76,9 @@ fp4attn_forward_options default_options() {
   o.affine_a = 1.5f;
   o.affine_b = 1.2f;
   o.ex2_pairs = 0;
+  o.guard = 0;
+  o.guard_margin = 110;
+  o.guard_shift = 16;
   return o;
 }
 
@@ -91,8 +94,23 @@ fp4attn_status check_options(const fp4attn_forward_options* opts, fp4attn_forwar
   const int k = opts->ex2_pairs;
   if (k != 0 && k != 1 && k != 2 && k != 4 && k != 8 && k != 16)
     return fail(FP4ATTN_ERR_INVALID_ARG, "ex2_pairs=%d is not one of 0, 1, 2, 4, 8, 16", k);
+  if (opts->guard != 0 && opts->guard != 1) return fail(FP4ATTN_ERR_INVALID_ARG, "guard must be 0 or 1");
+  if (opts->guard) {
+    if (opts->guard_margin < 0 || opts->guard_shift < 0 || opts->guard_margin + opts->guard_shift > 126)
+      return fail(FP4ATTN_ERR_INVALID_ARG, "guard margin %d and shift %d must be >= 0 with margin + shift <= 126",
+                  opts->guard_margin, opts->guard_shift);
+    if (k != 0 && k != 4 && k != 16)
+      return fail(FP4ATTN_ERR_UNSUPPORTED, "the guarded forward is built for ex2_pairs 0, 4 and 16, not %d", k);
+  }
   *out = *opts;
   return FP4ATTN_OK;
+}
+
+void set_options(fp4attn::DirectPArgs& a, const fp4attn_forward_options& o) {
+  a.ex2_pairs = o.ex2_pairs;
+  a.guard = o.guard;
+  a.guard_margin = o.guard_margin;
+  a.guard_shift = o.guard_shift;
 }
 
 fp4attn::DirectPArgs directp_args(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
@@ -118,12 +136,8 @@ fp4attn::DirectPArgs directp_args(const uint8_t* q_codes, const uint8_t* q_scale
   return a;
 }
 
-}  // namespace
-
-extern "C" {
-
-fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols,
-                                      int axis, uint8_t* codes, uint8_t* scales, void* stream) {
+fp4attn_status quantize_common(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
+                               int64_t n_anchor, uint8_t* codes, uint8_t* scales, void* stream) {
   REQUIRE_PTR(src);
   REQUIRE_PTR(codes);
   REQUIRE_PTR(scales);
@@ -138,9 +152,27 @@ fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t ba
     return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large");
   if ((batch * other * (blocked / 32) + 255) / 256 > 0x7fffffff)
     return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large for one launch");
-  return from_hip(fp4attn::launch_quantize_mxfp4(src, src_dtype, batch, rows, cols, axis, codes, scales,
+  return from_hip(fp4attn::launch_quantize_mxfp4(src, src_dtype, batch, rows, cols, axis, n_anchor, codes, scales,
                                                  static_cast<hipStream_t>(stream)),
                   "quantize launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols,
+                                      int axis, uint8_t* codes, uint8_t* scales, void* stream) {
+  return quantize_common(src, src_dtype, batch, rows, cols, axis, 0, codes, scales, stream);
+}
+
+fp4attn_status fp4attn_quantize_mxfp4_anchored(const void* src, int src_dtype, int64_t batch, int64_t rows,
+                                               int64_t cols, int axis, int64_t n_anchor, uint8_t* codes,
+                                               uint8_t* scales, void* stream) {
+  if (n_anchor < 1 || rows % n_anchor != 0)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "n_anchor=%lld must be >= 1 and divide rows=%lld", (long long)n_anchor,
+                (long long)rows);
+  return quantize_common(src, src_dtype, batch, rows, cols, axis, n_anchor, codes, scales, stream);
 }
 
 fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
@@ -172,7 +204,7 @@ fp4attn_status fp4attn_forward_mxfp4_ex(const uint8_t* q_codes, const uint8_t* q
   if (st != FP4ATTN_OK) return st;
   fp4attn::DirectPArgs a = directp_args(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
                                         softmax_scale, o.affine_a, o.affine_b, out, out_dtype);
-  a.ex2_pairs = o.ex2_pairs;
+  set_options(a, o);
   return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "forward launch");
 }
 
@@ -201,7 +233,7 @@ fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t
     return fail(FP4ATTN_ERR_INVALID_ARG, "wg_clock is not 16-byte aligned");
   fp4attn::DirectPArgs a = directp_args(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, B, H, N, d,
                                         softmax_scale, o.affine_a, o.affine_b, out, out_dtype);
-  a.ex2_pairs = o.ex2_pairs;
+  set_options(a, o);
   a.row_ids = n_rows > 0 ? row_ids : nullptr;
   a.n_rows = (int)n_rows;
   a.p_codes = p_codes;

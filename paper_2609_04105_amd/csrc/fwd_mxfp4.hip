@@ -1,37 +1,48 @@
 // Direct-P full-MXFP4 attention forward: host dispatch (the kernel and its
 // design are in fwd_mxfp4.hpp).  The EX2 = 0 variants are compiled here; the
-// native-exponential densities come from fwd_mxfp4_ex2*.hip, compiled in
-// parallel with this file.
+// native-exponential densities come from fwd_mxfp4_ex2*.hip and the guarded
+// variants from fwd_mxfp4_guard.hip, compiled in parallel with this file.
 #include "fwd_mxfp4.hpp"
 
 namespace fp4attn {
 namespace directp_detail {
 
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 0)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 1)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 2)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 8)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 0, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 1, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 2, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 8, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 0, true)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, true)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, true)
 
 namespace {
 
 template <int D, int NW, bool DUMP>
-hipError_t dispatch_ex2(const KParams& kp, int ex2, hipStream_t stream) {
+hipError_t dispatch_ex2(const KParams& kp, int ex2, bool guard, hipStream_t stream) {
+  if (guard) {
+    switch (ex2) {
+      case 0: return launch_directp<D, NW, DUMP, 0, true>(kp, stream);
+      case 4: return launch_directp<D, NW, DUMP, 4, true>(kp, stream);
+      case 16: return launch_directp<D, NW, DUMP, 16, true>(kp, stream);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (ex2) {
-    case 0: return launch_directp<D, NW, DUMP, 0>(kp, stream);
-    case 1: return launch_directp<D, NW, DUMP, 1>(kp, stream);
-    case 2: return launch_directp<D, NW, DUMP, 2>(kp, stream);
-    case 4: return launch_directp<D, NW, DUMP, 4>(kp, stream);
-    case 8: return launch_directp<D, NW, DUMP, 8>(kp, stream);
-    case 16: return launch_directp<D, NW, DUMP, 16>(kp, stream);
+    case 0: return launch_directp<D, NW, DUMP, 0, false>(kp, stream);
+    case 1: return launch_directp<D, NW, DUMP, 1, false>(kp, stream);
+    case 2: return launch_directp<D, NW, DUMP, 2, false>(kp, stream);
+    case 4: return launch_directp<D, NW, DUMP, 4, false>(kp, stream);
+    case 8: return launch_directp<D, NW, DUMP, 8, false>(kp, stream);
+    case 16: return launch_directp<D, NW, DUMP, 16, false>(kp, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int D, int NW>
-hipError_t dispatch_dump(const KParams& kp, bool dump, int ex2, hipStream_t stream) {
-  return dump ? dispatch_ex2<D, NW, true>(kp, ex2, stream) : dispatch_ex2<D, NW, false>(kp, ex2, stream);
+hipError_t dispatch_dump(const KParams& kp, bool dump, int ex2, bool guard, hipStream_t stream) {
+  return dump ? dispatch_ex2<D, NW, true>(kp, ex2, guard, stream) : dispatch_ex2<D, NW, false>(kp, ex2, guard, stream);
 }
 
 }  // namespace
@@ -57,6 +68,9 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   kp.k0_8 = k0 * 0.125f;
   kp.a8 = a.affine_a * 0.125f;
   kp.k1 = (float)kLog2Of6;
+  kp.margin = (float)a.guard_margin;
+  kp.floor_u = (float)(a.guard_shift + 1);
+  kp.shift = (float)a.guard_shift;
   kp.out_bf16 = a.out_bf16;
   kp.row_ids = a.row_ids;
   kp.n_rows = a.n_rows;
@@ -73,9 +87,11 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   kp.n_qtiles = a.N / BM;
   kp.total = kp.n_qtiles * bh;
   const int ex2 = a.ex2_pairs;
+  const bool guard = a.guard != 0;
   if (a.d == 128)
-    return wide ? dispatch_dump<128, 8>(kp, dump, ex2, stream) : dispatch_dump<128, 4>(kp, dump, ex2, stream);
-  return wide ? dispatch_dump<64, 8>(kp, dump, ex2, stream) : dispatch_dump<64, 4>(kp, dump, ex2, stream);
+    return wide ? dispatch_dump<128, 8>(kp, dump, ex2, guard, stream)
+                : dispatch_dump<128, 4>(kp, dump, ex2, guard, stream);
+  return wide ? dispatch_dump<64, 8>(kp, dump, ex2, guard, stream) : dispatch_dump<64, 4>(kp, dump, ex2, guard, stream);
 }
 
 }  // namespace fp4attn

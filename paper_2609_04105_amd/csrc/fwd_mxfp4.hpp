@@ -29,6 +29,10 @@
 // - Native-exponential mixing (template EX2 = k of the 16 pairs of a block):
 //   selected pairs take x = fma(c_y, raw, log2 6 - E_B) through v_exp_f32 and
 //   the converter with scale 1, i.e. the ideal code Q_E2M1(2^x).
+// - Sampled guard (template GUARD, Alg. 3): the row reference is fixed from
+//   the anchor keys of the first tile instead of following the block maxima;
+//   working bytes are floored at L + 1 before the codes are formed and
+//   published shifted down by L, so no rescale branch remains.
 // - Denominator c_B: an extra 16x16x128 product of the same P^T register with a
 //   constant indicator operand, so it uses exactly the codes and E8M0 bytes of
 //   PV and costs no vector-ALU work.
@@ -63,6 +67,7 @@ struct KParams {
   void* out;
   int N, n_qtiles, total;
   float c_y, c_a8, k0_8, a8, k1;
+  float margin, floor_u, shift;  // sampled guard: M, L + 1, L
   int out_bf16;
   const int64_t* row_ids;
   int n_rows;
@@ -176,7 +181,7 @@ struct TileRegs {
   }
 };
 
-template <int D, int NW, bool DUMP, int EX2>
+template <int D, int NW, bool DUMP, int EX2, bool GUARD>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_mxfp4_kernel(const KParams p) {
   static_assert(EX2 == 0 || EX2 == 1 || EX2 == 2 || EX2 == 4 || EX2 == 8 || EX2 == 16, "pairs per 32-key block");
   using L = Layout<D>;
@@ -239,6 +244,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   for (int c = 0; c < D / 32; ++c) O[c] = v16f{};
   v4f Dacc = v4f{};  // lane c < 16: register 0 = query c, register 1 = query c + 16
   float Mref = -1.0e6f;  // integer row reference (exact in fp32); no block seen yet
+  float Rref = 0.0f;     // guard: fixed row reference from the anchor tile (Alg. 3)
 
   const int ntiles = N / kBN;
   const int nsteps = 2 * ntiles;  // 64-key steps
@@ -299,9 +305,24 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 #pragma unroll
     for (int r = 1; r < 15; r += 2) m = fmaxf(fmaxf(m, acc[1][r]), acc[1][r + 1]);
     m = fmaxf(m, acc[1][15]);
-    const float E = floorf(m * p.c_y);          // block exponent (Alg. 2, step 2)
-    const float c0 = fmaf(-p.a8, E, p.k0_8);    // (A (log2 6 - E) + B) / 8
-    const float c1 = EX2 ? p.k1 - E : 0.0f;     // log2 6 - E, the exponent offset of 2^x
+    // Block exponent (Alg. 2, step 2) and the offset T of the code map,
+    // x = y - T + log2 6.  Online reference: T = E_B = floor(max y).  Guard
+    // (Alg. 3, step 3): e_B = floor(max y - R), working byte ubar_B =
+    // clamp(e_B + 127, L + 1, 254), T = R + ubar_B - 127 (every step rounded
+    // to fp32 on its own).
+    float E, T, ub = 0.0f;
+    if constexpr (GUARD) {
+#pragma clang fp contract(off)
+      const float Y = m * p.c_y;
+      ub = __builtin_amdgcn_fmed3f(floorf(Y - Rref) + 127.0f, p.floor_u, 254.0f);
+      E = ub - 127.0f;
+      T = Rref + E;
+    } else {
+      E = floorf(m * p.c_y);
+      T = E;
+    }
+    const float c0 = fmaf(-p.a8, T, p.k0_8);    // (A (log2 6 - T) + B) / 8
+    const float c1 = EX2 ? p.k1 - T : 0.0f;     // log2 6 - T, the exponent offset of 2^x
     // Code map on u / 8.  Every byte of the four words is written below; the
     // first convert of each word takes its own input as the overwritten value.
     unsigned w[4];
@@ -327,25 +348,37 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     // instead of letting it sink below the rescale branch (emits nothing).
     asm volatile("" ::"v"(P));
     if constexpr (decltype(SCHED_)::value) schedule_step();
-    // Online integer reference with a lazy, exact power-of-two rescale of what
-    // PV has accumulated so far; the halves agree on the reference because the
-    // branch is taken by the whole wave and uses both halves' exponents.
-    if (__builtin_amdgcn_ballot_w64(E > Mref + kTau)) {
-      unsigned ea = as_uint(E), eb = ea;
-      swap_halves(ea, eb);  // each lane: (block-0 exponent, block-1 exponent)
-      const float Emax = fmaxf(as_float(ea), as_float(eb));
-      const float Mn = Emax > Mref + kTau ? Emax : Mref;
-      const int sh = (int)(Mref - Mn);
+    if constexpr (GUARD) {
+      // published byte ubar_B - L, in [1, 254 - L]
+      u = (int)__builtin_amdgcn_cvt_pk_u8_f32(ub - p.shift, 0, 0u);
+      // The rescale branch of the online reference is where the accumulators
+      // pass between steps; without it the compiler regroups the PV chains of
+      // several steps and runs out of registers.  Pass them through here
+      // (emits nothing).
 #pragma unroll
-      for (int c = 0; c < D / 32; ++c)
+      for (int c = 0; c < D / 32; ++c) asm volatile("" : "+v"(O[c]));
+      asm volatile("" : "+v"(Dacc));
+    } else {
+      // Online integer reference with a lazy, exact power-of-two rescale of what
+      // PV has accumulated so far; the halves agree on the reference because the
+      // branch is taken by the whole wave and uses both halves' exponents.
+      if (__builtin_amdgcn_ballot_w64(E > Mref + kTau)) {
+        unsigned ea = as_uint(E), eb = ea;
+        swap_halves(ea, eb);  // each lane: (block-0 exponent, block-1 exponent)
+        const float Emax = fmaxf(as_float(ea), as_float(eb));
+        const float Mn = Emax > Mref + kTau ? Emax : Mref;
+        const int sh = (int)(Mref - Mn);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
-      Dacc[0] = ldexpf(Dacc[0], sh);
-      Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
-      Mref = Mn;
+        for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
+        Dacc[0] = ldexpf(Dacc[0], sh);
+        Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
+        Mref = Mn;
+      }
+      // E8M0 byte of this lane's block: clamp(E - M + 127, 0, 254) (E - M <= kTau).
+      u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mref + 127.0f, 0, 0u);
     }
-    // E8M0 byte of this lane's block: clamp(E - M + 127, 0, 254) (E - M <= kTau).
-    u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mref + 127.0f, 0, 0u);
     if constexpr (DUMP) {
       if (slot >= 0) {
         const int kb = 2 * g + h;
@@ -381,9 +414,29 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   v16f SA[2], SB[2];
   v4i PA, PB;
   int uA, uB;
-  qk(lds, std::integral_constant<int, 0>{}, SA);
-  directp(SA, 0, PA, uA, std::false_type{});
-  qk(lds, std::integral_constant<int, 1>{}, SA);
+  if constexpr (GUARD) {
+    // Anchor (Alg. 3, steps 1-2): the largest score of the first key tile, which
+    // holds the anchor keys; each lane half has two of its four 32-key blocks.
+    qk(lds, std::integral_constant<int, 0>{}, SB);
+    qk(lds, std::integral_constant<int, 1>{}, SA);
+    float am = fmaxf(SB[0][0], SB[1][0]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, SB[0][r]), SB[1][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, SA[0][r]), SA[1][r]);
+    unsigned ma = as_uint(am), mb = ma;
+    swap_halves(ma, mb);
+    {
+#pragma clang fp contract(off)
+      const float Y = fmaxf(as_float(ma), as_float(mb)) * p.c_y;
+      Rref = Y + p.margin;
+    }
+    directp(SB, 0, PA, uA, std::false_type{});
+  } else {
+    qk(lds, std::integral_constant<int, 0>{}, SA);
+    directp(SA, 0, PA, uA, std::false_type{});
+    qk(lds, std::integral_constant<int, 1>{}, SA);
+  }
 
   // One step of the pipeline; j is the step's position in its group of eight.
   // GUARD: the tail group, where QK, Direct-P or the step itself may not exist.
@@ -454,7 +507,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   }
   if constexpr (DUMP) {
     if (slot >= 0 && h == 0) {
-      p.row_m[slot] = (int)Mref;
+      p.row_m[slot] = GUARD ? 0 : (int)Mref;
       p.row_d[slot] = Dfin;
     }
   }
@@ -466,27 +519,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   }
 }
 
-template <int D, int NW, bool DUMP, int EX2>
+template <int D, int NW, bool DUMP, int EX2, bool GUARD>
 hipError_t launch_directp(const KParams& kp, hipStream_t stream) {
-  hipLaunchKernelGGL((fwd_mxfp4_kernel<D, NW, DUMP, EX2>), dim3(kp.total), dim3(NW * 64), 0, stream, kp);
+  hipLaunchKernelGGL((fwd_mxfp4_kernel<D, NW, DUMP, EX2, GUARD>), dim3(kp.total), dim3(NW * 64), 0, stream, kp);
   return hipGetLastError();
 }
 
-// Every (D, NW, DUMP) variant of one EX2 density.
-#define FP4ATTN_DIRECTP_VARIANTS(MACRO, EX2) \
-  MACRO(64, 4, false, EX2)                   \
-  MACRO(64, 4, true, EX2)                    \
-  MACRO(64, 8, false, EX2)                   \
-  MACRO(64, 8, true, EX2)                    \
-  MACRO(128, 4, false, EX2)                  \
-  MACRO(128, 4, true, EX2)                   \
-  MACRO(128, 8, false, EX2)                  \
-  MACRO(128, 8, true, EX2)
+// Every (D, NW, DUMP) variant of one EX2 density and reference mode.
+#define FP4ATTN_DIRECTP_VARIANTS(MACRO, EX2, GUARD) \
+  MACRO(64, 4, false, EX2, GUARD)                   \
+  MACRO(64, 4, true, EX2, GUARD)                    \
+  MACRO(64, 8, false, EX2, GUARD)                   \
+  MACRO(64, 8, true, EX2, GUARD)                    \
+  MACRO(128, 4, false, EX2, GUARD)                  \
+  MACRO(128, 4, true, EX2, GUARD)                   \
+  MACRO(128, 8, false, EX2, GUARD)                  \
+  MACRO(128, 8, true, EX2, GUARD)
 
-#define FP4ATTN_DIRECTP_DECLARE(D, NW, DUMP, EX2) \
-  extern template hipError_t launch_directp<D, NW, DUMP, EX2>(const KParams&, hipStream_t);
-#define FP4ATTN_DIRECTP_DEFINE(D, NW, DUMP, EX2) \
-  template hipError_t launch_directp<D, NW, DUMP, EX2>(const KParams&, hipStream_t);
+#define FP4ATTN_DIRECTP_DECLARE(D, NW, DUMP, EX2, GUARD) \
+  extern template hipError_t launch_directp<D, NW, DUMP, EX2, GUARD>(const KParams&, hipStream_t);
+#define FP4ATTN_DIRECTP_DEFINE(D, NW, DUMP, EX2, GUARD) \
+  template hipError_t launch_directp<D, NW, DUMP, EX2, GUARD>(const KParams&, hipStream_t);
 
 }  // namespace directp_detail
 }  // namespace fp4attn

@@ -8,8 +8,9 @@
 
 namespace fp4attn {
 
+// n_anchor > 0: rows are read in anchor order (rows % n_anchor == 0).
 hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
-                                 uint8_t* codes, uint8_t* scales, hipStream_t stream);
+                                 int64_t n_anchor, uint8_t* codes, uint8_t* scales, hipStream_t stream);
 
 hipError_t launch_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols, void* dst,
                                  hipStream_t stream);
@@ -26,6 +27,8 @@ struct DirectPArgs {
   int out_bf16;
   float softmax_scale, affine_a, affine_b;
   int ex2_pairs;  // pairs of 16 per 32-key block that take the native exponential
+  int guard;      // sampled anchor reference (Alg. 3) instead of the online one
+  int guard_margin, guard_shift;
   // test hook (all null / zero for the plain forward)
   const int64_t* row_ids;
   int n_rows;

@@ -32,12 +32,24 @@ __device__ __forceinline__ float load_as_float<uint16_t>(const uint16_t* p) {
   return __builtin_bit_cast(float, (unsigned)(*p) << 16);
 }
 
+// Source row of row r of the anchor-ordered matrix (Sec. "Fix 3": the anchor
+// rows j * stride, j < n_anchor, first, then every other row in order);
+// stride 0 is the identity.  Always within [0, n_anchor * stride).
+__device__ __forceinline__ int64_t anchor_source_row(int64_t r, int64_t n_anchor, int64_t stride) {
+  if (stride <= 1) return r;
+  if (r < n_anchor) return r * stride;
+  const int64_t k = r - n_anchor;
+  return (k / (stride - 1)) * stride + 1 + k % (stride - 1);
+}
+
 // axis == 1: blocks along the contiguous axis (Q, K).  axis == 0: blocks along
-// rows, output transposed (V).
+// rows, output transposed (V).  Rows are read in anchor order when
+// anchor_stride > 0.
 template <typename T, int AXIS>
 __global__ __launch_bounds__(256) void quantize_mxfp4_kernel(const T* __restrict__ src, int64_t batch, int64_t rows,
                                                              int64_t cols, uint8_t* __restrict__ codes,
-                                                             uint8_t* __restrict__ scales) {
+                                                             uint8_t* __restrict__ scales, int64_t n_anchor,
+                                                             int64_t anchor_stride) {
   const int64_t nblk = AXIS == 1 ? cols / 32 : rows / 32;
   const int64_t outer = AXIS == 1 ? rows : cols;
   const int64_t total = batch * outer * nblk;
@@ -55,13 +67,17 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_kernel(const T* __restrict
   }
   float v[32];
   if (AXIS == 1) {
-    const T* p = src + (b * rows + o) * cols + blk * 32;
+    const T* p = src + (b * rows + anchor_source_row(o, n_anchor, anchor_stride)) * cols + blk * 32;
 #pragma unroll
     for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + j);
-  } else {
+  } else if (anchor_stride <= 1) {
     const T* p = src + (b * rows + blk * 32) * cols + o;
 #pragma unroll
     for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + (int64_t)j * cols);
+  } else {
+    const T* p = src + b * rows * cols + o;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + anchor_source_row(blk * 32 + j, n_anchor, anchor_stride) * cols);
   }
   float amax = 0.0f;
   bool finite = true;
@@ -127,7 +143,8 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __r
 }
 
 hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
-                                 uint8_t* codes, uint8_t* scales, hipStream_t stream) {
+                                 int64_t n_anchor, uint8_t* codes, uint8_t* scales, hipStream_t stream) {
+  const int64_t stride = n_anchor > 0 ? rows / n_anchor : 0;
   const int64_t nblk = axis == 1 ? cols / 32 : rows / 32;
   const int64_t outer = axis == 1 ? rows : cols;
   const int64_t total = batch * outer * nblk;
@@ -135,17 +152,17 @@ hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, 
   if (src_dtype == 0) {
     if (axis == 1)
       hipLaunchKernelGGL((quantize_mxfp4_kernel<float, 1>), grid, block, 0, stream, (const float*)src, batch, rows,
-                         cols, codes, scales);
+                         cols, codes, scales, n_anchor, stride);
     else
       hipLaunchKernelGGL((quantize_mxfp4_kernel<float, 0>), grid, block, 0, stream, (const float*)src, batch, rows,
-                         cols, codes, scales);
+                         cols, codes, scales, n_anchor, stride);
   } else {
     if (axis == 1)
       hipLaunchKernelGGL((quantize_mxfp4_kernel<uint16_t, 1>), grid, block, 0, stream, (const uint16_t*)src, batch,
-                         rows, cols, codes, scales);
+                         rows, cols, codes, scales, n_anchor, stride);
     else
       hipLaunchKernelGGL((quantize_mxfp4_kernel<uint16_t, 0>), grid, block, 0, stream, (const uint16_t*)src, batch,
-                         rows, cols, codes, scales);
+                         rows, cols, codes, scales, n_anchor, stride);
   }
   return hipGetLastError();
 }

@@ -83,3 +83,45 @@ def check_directp_dump(dump, ref, label):
     rel = np.abs(D - ref["D"]) / ref["D"]
     assert rel.max() < 1e-4, f"{label}: denominator rel error {rel.max():.3e}"
     return mismatch
+
+
+def oracle_rows_guarded(q, k, v, rows, softmax_scale, margin, shift, ex2_pairs=0):
+    """The guarded oracle (Alg. 3) on flattened query ``rows`` of fp64 q, k, v
+    [B, H, N, d] in their ORIGINAL key order: K and V are put in anchor order
+    here, as the anchored quantizer does on the GPU."""
+    from oracle import guard
+    B, H, N, d = q.shape
+    perm = guard.anchor_permutation(N)
+    rows = np.asarray(rows, dtype=np.int64)
+    heads = rows // N
+    out = {"O": np.zeros((len(rows), d)), "ebar": np.zeros((len(rows), N // 32), dtype=np.int64),
+           "D": np.zeros(len(rows)), "codes": np.zeros((len(rows), N), dtype=np.uint8)}
+    for bh in np.unique(heads):
+        b, h = divmod(int(bh), H)
+        sel = np.nonzero(heads == bh)[0]
+        local = rows[sel] % N
+        qc, qs = mxfp4.quantize(q[b, h][local], axis=-1)
+        kc, ks = mxfp4.quantize(k[b, h][perm], axis=-1)
+        vc, vs = mxfp4.quantize(v[b, h][perm], axis=-2)
+        res = guard.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(local)), softmax_scale, margin, shift,
+                                 ex2_pairs=ex2_pairs)
+        for key in out:
+            out[key][sel] = res[key]
+    return out
+
+
+def check_guarded_dump(dump, ref, label):
+    """Assert the guarded Direct-P dump against the oracle: codes, working exponents
+    (decided in the same fp32 steps, so exact), and the denominator."""
+    codes = unpack_codes(dump["p_codes"].cpu().numpy())
+    mag = codes & 7
+    assert not np.any(((codes & 8) != 0) & (mag != 0)), f"{label}: a nonzero P code carries a sign bit"
+    mismatch = float(np.mean(mag != ref["codes"]))
+    assert mismatch <= CODE_MISMATCH_MAX, f"{label}: code mismatch fraction {mismatch:.3e}"
+    E = dump["block_exp"].cpu().numpy().astype(np.int64)
+    assert np.array_equal(E, ref["ebar"]), f"{label}: working exponents differ"
+    assert np.all(dump["row_m"].cpu().numpy() == 0)
+    D = dump["row_d"].cpu().numpy().astype(np.float64)
+    rel = np.abs(D - ref["D"]) / ref["D"]
+    assert rel.max() < 1e-4, f"{label}: denominator rel error {rel.max():.3e}"
+    return mismatch

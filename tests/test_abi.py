@@ -72,6 +72,10 @@ def test_quantize_and_bf16_validation(lib):
     assert q(FAKE[0], 2, 1, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # dtype
     assert q(FAKE[0], 0, 1, 4, 64, 2, FAKE[1], FAKE[2], None) == 1     # axis
     assert q(FAKE[0], 0, 0, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # batch
+    qa = lib.fp4attn_quantize_mxfp4_anchored
+    assert qa(FAKE[0], 0, 1, 256, 64, 1, 0, FAKE[1], FAKE[2], None) == 1     # n_anchor < 1
+    assert qa(FAKE[0], 0, 1, 256, 64, 1, 96, FAKE[1], FAKE[2], None) == 1    # does not divide rows
+    assert qa(FAKE[0], 0, 1, 256, 64, 2, 128, FAKE[1], FAKE[2], None) == 1   # axis
     b = lib.fp4attn_forward_bf16
     assert b(*FAKE[:3], 1, 1, 128, 80, 0.125, FAKE[4], 0, None) == 2
     assert b(None, *FAKE[1:3], 1, 1, 128, 64, 0.125, FAKE[4], 0, None) == 1
@@ -86,9 +90,10 @@ def test_quantize_and_bf16_validation(lib):
 def test_forward_options(lib):
     from paper_2609_04105_amd import _lib
     o = _lib.ForwardOptions()
-    assert ctypes.sizeof(o) == 16
+    assert ctypes.sizeof(o) == 28
     lib.fp4attn_forward_options_init(ctypes.byref(o))
-    assert (o.struct_size, o.affine_a, o.ex2_pairs) == (16, 1.5, 0) and abs(o.affine_b - 1.2) < 1e-6
+    assert (o.struct_size, o.affine_a, o.ex2_pairs) == (28, 1.5, 0) and abs(o.affine_b - 1.2) < 1e-6
+    assert (o.guard, o.guard_margin, o.guard_shift) == (0, 110, 16)
     e = lib.fp4attn_forward_mxfp4_ex
     for kx in (3, 5, 32, -1):
         o.ex2_pairs = kx
@@ -96,7 +101,17 @@ def test_forward_options(lib):
     o.ex2_pairs = 4
     o.struct_size = 12
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
-    o.struct_size = 16
+    o.struct_size = 28
+    o.guard = 1
+    for M, L in ((110, 17), (-1, 0), (0, -1)):
+        o.guard_margin, o.guard_shift = M, L
+        assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
+    o.guard_margin, o.guard_shift = 110, 16
+    o.ex2_pairs = 2
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 2     # guard: 0, 4, 16 only
+    o.guard, o.ex2_pairs = 2, 4
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
+    o.guard = 0
     o.affine_a = 0.0
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
     o.affine_a = 1.5

@@ -214,3 +214,91 @@ def test_ex2_density_fidelity_against_exact_attention(fa):
         print(f"[fidelity] ex2_pairs={kx:2d} cos {cos:.6f} rel-L2 {rel:.6f} RMSE {rmse:.6f}", flush=True)
         rels.append(rel)
     assert all(a > b for a, b in zip(rels, rels[1:])), rels
+
+
+# ---- sampled QK guard (Alg. 3) ------------------------------------------------------------
+
+def _run_guarded(fa, host64, dev, rows, label, margin, shift, ex2_pairs=0, softmax_scale=None):
+    from parity import check_guarded_dump, oracle_rows_guarded
+    q, k, v = host64
+    B, H, N, d = q.shape
+    s = 1.0 / np.sqrt(d) if softmax_scale is None else softmax_scale
+    ops = fa.quantize_qkv(*dev, anchored=True)
+    row_ids = torch.from_numpy(np.asarray(rows, dtype=np.int64)).cuda()
+    print(f"[{label}] guard M={margin} L={shift} ex2={ex2_pairs} B{B} H{H} N{N} d{d} rows={len(rows)}", flush=True)
+    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, ex2_pairs=ex2_pairs, guard=(margin, shift))
+    out = fa.forward_mxfp4(*ops, softmax_scale=s, ex2_pairs=ex2_pairs, guard=(margin, shift))
+    torch.cuda.synchronize()
+    assert torch.equal(out, dump["out"])
+    ref = oracle_rows_guarded(q, k, v, rows, s, margin, shift, ex2_pairs)
+    mismatch = check_guarded_dump(dump, ref, label)
+    got = out.reshape(-1, d)[torch.from_numpy(np.asarray(rows)).cuda()].cpu().numpy()
+    assert np.all(np.isfinite(got))
+    rel, cos = rel_l2_cos(got, ref["O"])
+    print(f"[{label}] code mismatch {mismatch:.2e}  O rel-L2 {rel:.3e}  cos {cos:.8f}", flush=True)
+    assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{label}: rel {rel} cos {cos}"
+
+
+@pytest.mark.parametrize("margin,shift", [(8, 0), (20, 16), (110, 16), (112, 14)])
+def test_guard_small_all_rows(fa, margin, shift):
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    _run_guarded(fa, host64, dev, workloads.sampled_rows("small_b1h8_n1024_d64"), "small", margin, shift)
+
+
+@pytest.mark.parametrize("ex2_pairs", [4, 16])
+def test_guard_with_native_exponential_pairs(fa, ex2_pairs):
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    _run_guarded(fa, host64, dev, workloads.sampled_rows("small_b1h8_n1024_d64"), "small", 110, 16, ex2_pairs)
+
+
+@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "long_b1h32_n16384_d128"])
+def test_guard_full_size_sampled_rows(fa, name):
+    host64, dev = load_workload(name)
+    _run_guarded(fa, host64, dev, workloads.sampled_rows(name), name, 110, 16)
+
+
+def test_guard_tiny_and_ragged(fa):
+    host64, dev = load_workload("tiny_b1h1_n128_d64")
+    _run_guarded(fa, host64, dev, np.arange(128), "tiny", 110, 16)
+    g = torch.Generator().manual_seed(33)
+    q, k, v = (torch.randn(1, 2, 1152, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    _run_guarded(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(2 * 1152), "ragged N1152", 20, 16)
+
+
+def test_guard_extreme_logits(fa):
+    """Logits in the thousands (the regime the guard serves): finite output that
+    matches the oracle."""
+    g = torch.Generator().manual_seed(34)
+    q = (torch.randn(1, 2, 512, 64, generator=g) * 60).to(torch.bfloat16)
+    k = (torch.randn(1, 2, 512, 64, generator=g) * 4).to(torch.bfloat16)
+    v = torch.randn(1, 2, 512, 64, generator=g).to(torch.bfloat16)
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    _run_guarded(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(1024), "extreme", 110, 16)
+
+
+def test_guard_fidelity_against_exact_attention(fa):
+    """Operator error of the guarded route against exact attention (4096 sampled rows
+    of the long workload): with a small margin it equals the online route's; the
+    paper's (110, 16) floors sub-anchor blocks of these flat Gaussian rows."""
+    from oracle import exact
+    name = "long_b1h32_n16384_d128"
+    (q, k, v), dev = load_workload(name)
+    rows = workloads.sampled_rows(name)
+    B, H, N, d = q.shape
+    s = 1.0 / np.sqrt(d)
+    ref = np.zeros((len(rows), d))
+    for bh in np.unique(rows // N):
+        sel = np.nonzero(rows // N == bh)[0]
+        b, h = divmod(int(bh), H)
+        ref[sel] = exact.attention(q[b, h][rows[sel] % N], k[b, h], v[b, h], s)
+    idx = torch.from_numpy(rows).cuda()
+    online = fa.forward_mxfp4(*gpu_operands(*dev)).reshape(-1, d)[idx].cpu().numpy()
+    anch = fa.quantize_qkv(*dev, anchored=True)
+    rel = {"online": exact.error_metrics(online, ref)[1]}
+    for ml in ((8, 0), (110, 16)):
+        got = fa.forward_mxfp4(*anch, guard=ml).reshape(-1, d)[idx].cpu().numpy()
+        cos, rel[ml], rmse = exact.error_metrics(got, ref)
+        print(f"[fidelity] guard M={ml[0]} L={ml[1]}: cos {cos:.6f} rel-L2 {rel[ml]:.6f} RMSE {rmse:.6f}", flush=True)
+    print(f"[fidelity] online reference: rel-L2 {rel['online']:.6f}", flush=True)
+    assert abs(rel[(8, 0)] / rel["online"] - 1) < 0.05

@@ -88,3 +88,17 @@ def test_workload_operands(fa, name):
         bb, hh = divmod(bh, w.H)
         c_ref, s_ref = mxfp4.quantize(workloads.as_f64(v[bb, hh]), axis=-2)
         assert np.array_equal(host[4][bb, hh], c_ref) and np.array_equal(host[5][bb, hh], s_ref)
+
+
+@pytest.mark.parametrize("axis", [-1, -2])
+@pytest.mark.parametrize("rows", [128, 1024, 4096])
+def test_anchor_order(fa, axis, rows):
+    """fp4attn_quantize_mxfp4_anchored equals the plain quantizer applied to the
+    rows in the oracle's anchor order (Sec. "Fix 3")."""
+    from oracle import guard
+    g = torch.Generator().manual_seed(rows + 7 * axis)
+    x = torch.randn(2, rows, 64, generator=g).to(torch.bfloat16)
+    perm = guard.anchor_permutation(rows)
+    cg, sg = fa.quantize_mxfp4(x.cuda(), axis=axis, n_anchor=128)
+    co, so = mxfp4.quantize(workloads.as_f64(x)[:, perm], axis=axis)
+    assert np.array_equal(sg.cpu().numpy(), so) and np.array_equal(cg.cpu().numpy(), co)
