@@ -45,6 +45,15 @@ represented-contributions, represented-output):
 6. Output (eq. represented-output): ``O_i = sum_B w_B sum_j q_ij Vhat_j / D_i``
    in fp64, with ``Vhat`` the represented MXFP4 value of V (blocks of 32 keys).
 
+Causal form (the forward of the paper's causal-training route, Sec. "Pass the
+forward quantization into backward"): query i sees keys j <= i only.  Masked
+scores are -inf: they take code 0, a block with no visible key has no block
+exponent (weight 0), and ``M_i`` is the largest exponent over visible blocks.
+The saved row normaliser is the natural-log log-sum-exp of the represented
+operator, ``LSE_i = M_i ln 2 + ln(D_i / 6)``: with ``2**E_B q_ij / 6`` standing
+for ``exp(z_ij)``, ``exp(z_ij - LSE_i)`` is the represented probability
+``w_B q_ij / D_i`` that the backward reconstructs.
+
 The online (tiled) form keeps a running integer reference and rescales by
 exact powers of two (eq. online-recurrence with ``e**(m - m')`` replaced by
 ``2**(M - M')``); it gives the same codes and, up to fp64 rounding, the same
@@ -60,6 +69,9 @@ LOG2_6 = 2.584962500721156
 
 BLOCK = 32
 MODES = ("affine32", "affine64", "exp2", "exp2_exact")
+NO_BLOCK = -(1 << 40)   # block exponent of a block with no visible key (causal mask)
+LN_2 = 0.6931471805599453
+LN_6 = 1.791759469228055
 EX2_PAIRS = (0, 1, 2, 4, 8, 16)
 
 
@@ -98,13 +110,20 @@ def raw_scores(q6, k6):
     return raw
 
 
-def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affine32", ex2_pairs=0):
+def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affine32", ex2_pairs=0,
+                              visible=None):
     """(E [R, N/32] int64, q [R, N] fp64 magnitudes, k [R, N] uint8 code indices or None).
 
     ``raw`` is the [R, N] score matrix of step 1.  For ``exp2_exact`` the
     returned ``q`` holds the unrounded ``2**x`` and ``k`` is None.
     ``ex2_pairs`` (mode ``affine32`` only) selects native-exponential mixing.
+    ``visible`` ([R, N] bool, causal mask): hidden scores get code 0 and a block
+    without visible keys gets ``E = NO_BLOCK``.
     """
+    if visible is not None:
+        E, q, k = block_exponents_and_codes(np.where(visible, raw, -np.inf), softmax_scale, affine_a, affine_b,
+                                            mode, ex2_pairs)
+        return E, np.where(visible, q, 0.0), (None if k is None else np.where(visible, k, 0).astype(np.uint8))
     if mode not in MODES:
         raise ValueError(f"mode must be one of {MODES}")
     mask = ex2_key_mask(ex2_pairs)
@@ -118,14 +137,14 @@ def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affi
         c_y, c_a, k0 = fp32_coefficients(softmax_scale, affine_a, affine_b)
         raw32 = raw.astype(np.float32)
         y = fp32.mul(raw32, c_y)
-        E = np.floor(y.reshape(R, nb, BLOCK).max(axis=-1).astype(np.float64)).astype(np.int64)
+        E = _floor_exponent(y.reshape(R, nb, BLOCK).max(axis=-1).astype(np.float64))
         a32 = np.float32(affine_a)
-        c0 = fp32.fma(-a32, E.astype(np.float32), k0)
+        c0 = fp32.fma(-a32, _finite(E).astype(np.float32), k0)
         u = fp32.fma(c_a, raw32, np.repeat(c0, BLOCK, axis=-1)).astype(np.float64)
         k = e2m1.round_index(np.maximum(u, 0.0))
         if ex2_pairs:
             k1 = np.float32(LOG2_6)
-            c1 = fp32.fma(np.float32(-1.0), E.astype(np.float32), k1)       # fp32(k1 - E_B)
+            c1 = fp32.fma(np.float32(-1.0), _finite(E).astype(np.float32), k1)  # fp32(k1 - E_B)
             x = fp32.fma(c_y, raw32, np.repeat(c1, BLOCK, axis=-1))
             p = np.exp2(x.astype(np.float64)).astype(np.float32).astype(np.float64)
             keys = np.tile(mask, nb)
@@ -134,8 +153,8 @@ def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affi
     # fp64 modes follow eq. ideal-code-path / affine-code-map literally.
     s = float(np.float32(softmax_scale))
     y = raw * (s / 36.0) * LOG2_E
-    E = np.floor(y.reshape(R, nb, BLOCK).max(axis=-1)).astype(np.int64)
-    x = y - np.repeat(E, BLOCK, axis=-1) + LOG2_6
+    E = _floor_exponent(y.reshape(R, nb, BLOCK).max(axis=-1))
+    x = y - np.repeat(_finite(E), BLOCK, axis=-1) + LOG2_6
     if mode == "affine64":
         a = float(np.float32(affine_a))
         b = float(np.float32(affine_b))
@@ -148,11 +167,27 @@ def block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode="affi
     return E, p, None
 
 
+def _floor_exponent(ymax):
+    """floor of the block maxima; NO_BLOCK where a block has no finite score."""
+    with np.errstate(invalid="ignore"):
+        return np.where(np.isfinite(ymax), np.floor(np.nan_to_num(ymax, neginf=0.0)), NO_BLOCK).astype(np.int64)
+
+
+def _finite(E):
+    """Block exponents with NO_BLOCK replaced by 0 (the codes of such blocks are all 0 anyway)."""
+    return np.where(E == NO_BLOCK, 0, E)
+
+
+def lse(M, D):
+    """Natural-log row normaliser of the represented operator: M ln 2 + ln(D / 6)."""
+    return np.asarray(M, dtype=np.float64) * LN_2 + np.log(np.asarray(D, dtype=np.float64)) - LN_6
+
+
 def _normalise(E, q, v6, M):
     """Steps 4-6 for one row chunk: (D relative to 2**M, O)."""
     R, N = q.shape
     nb = N // BLOCK
-    w = np.ldexp(1.0, E - M[:, None])                        # 2**(E_B - M_i), exact
+    w = np.ldexp(1.0, np.maximum(E - M[:, None], -2000))    # 2**(E_B - M_i), exact (0 for NO_BLOCK)
     c = q.reshape(R, nb, BLOCK).sum(axis=-1)                 # c_B = sum_j q_ij
     D = (w * c).sum(axis=-1)                                 # represented denominator
     acc = (q * np.repeat(w, BLOCK, axis=-1)) @ v6            # sum_B w_B sum_j q_ij (6 Vhat_j)
@@ -162,30 +197,33 @@ def _normalise(E, q, v6, M):
 
 def forward_rows(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, rows,
                  softmax_scale, affine_a=1.5, affine_b=1.2, mode="affine32",
-                 chunk=128, want_codes=True, ex2_pairs=0):
+                 chunk=128, want_codes=True, ex2_pairs=0, causal=False):
     """Direct-P forward for the query ``rows`` of ONE (batch, head) slice.
 
     Operands are single-head MXFP4 arrays as produced by :func:`oracle.mxfp4.quantize`:
     q/k codes [N, d/2] + scales [N, d/32]; vt codes [d, N/2] + scales [d, N/32].
     Returns a dict with ``E`` [R, N/32] (absolute block exponents), ``M`` [R]
     (integer row reference), ``D`` [R] (denominator relative to 2**M), ``O``
-    [R, d] (fp64), and when ``want_codes`` ``codes`` [R, N] (E2M1 magnitude
-    indices 0..7; for ``exp2_exact`` the unrounded values instead).
+    [R, d] (fp64), ``LSE`` [R] (natural log), and when ``want_codes`` ``codes``
+    [R, N] (E2M1 magnitude indices 0..7; for ``exp2_exact`` the unrounded
+    values instead).  ``causal``: row ``rows[r]`` sees keys ``j <= rows[r]``.
     """
     rows = np.asarray(rows, dtype=np.int64)
     q6 = mxfp4.scaled_operand(q_codes, q_scales)[rows]
     k6 = mxfp4.scaled_operand(k_codes, k_scales)
     v6 = mxfp4.scaled_operand(vt_codes, vt_scales).T         # [N, d], 6 * Vhat
-    out = {"E": [], "M": [], "D": [], "O": [], "codes": []}
+    out = {"E": [], "M": [], "D": [], "O": [], "LSE": [], "codes": []}
     for lo in range(0, len(rows), chunk):
         raw = raw_scores(q6[lo:lo + chunk], k6)
-        E, q, k = block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode, ex2_pairs)
+        vis = (np.arange(raw.shape[1])[None, :] <= rows[lo:lo + chunk, None]) if causal else None
+        E, q, k = block_exponents_and_codes(raw, softmax_scale, affine_a, affine_b, mode, ex2_pairs, vis)
         M = E.max(axis=-1)
         D, O = _normalise(E, q, v6, M)
         out["E"].append(E)
         out["M"].append(M)
         out["D"].append(D)
         out["O"].append(O)
+        out["LSE"].append(lse(M, D))
         if want_codes:
             out["codes"].append(k if k is not None else q)
     res = {key: np.concatenate(val) for key, val in out.items() if val}
@@ -237,7 +275,7 @@ def p_scale_bytes(E, M):
 def represented_probabilities(E, q, M):
     """Normalised represented probabilities ``w_B q_ij / D_i`` [R, N] (rows sum to 1)."""
     R, N = q.shape
-    w = np.repeat(np.ldexp(1.0, np.asarray(E) - np.asarray(M)[:, None]), BLOCK, axis=-1)
+    w = np.repeat(np.ldexp(1.0, np.maximum(np.asarray(E) - np.asarray(M)[:, None], -2000)), BLOCK, axis=-1)
     num = w * q
     return num / num.sum(axis=-1, keepdims=True)
 

@@ -17,11 +17,13 @@ f64 = np.float64
 
 
 def _two_sum(a, b):
-    """s, e with s = fl64(a + b) and s + e = a + b exactly (Knuth)."""
+    """s, e with s = fl64(a + b) and s + e = a + b exactly (Knuth); e = 0 where s
+    is infinite (masked scores enter as -inf)."""
     s = a + b
-    bb = s - a
-    e = (a - (s - bb)) + (b - bb)
-    return s, e
+    with np.errstate(invalid="ignore"):
+        bb = s - a
+        e = (a - (s - bb)) + (b - bb)
+    return s, np.where(np.isfinite(s), e, 0.0)
 
 
 def round_to_f32(s, e):

@@ -300,3 +300,81 @@ def test_ex2_block_argmax_gets_code_six(gaussian_head_d128):
     _, _, kk = directp.block_exponents_and_codes(raw, s, 1.5, 1.2, ex2_pairs=16)
     am = raw.reshape(64, -1, 32).argmax(axis=-1)
     assert np.all(np.take_along_axis(kk.reshape(64, -1, 32), am[..., None], -1) == 7)
+
+
+# ---- causal form and the saved row normaliser ----------------------------------------------
+
+def _scores_natural(ops, rows, s):
+    q6 = mxfp4.scaled_operand(*ops[0:2])[rows]
+    k6 = mxfp4.scaled_operand(*ops[2:4])
+    return (q6 @ k6.T) * (s / 36.0)                          # z = s Qhat.Khat
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_lse_of_unrounded_codes_is_the_textbook_logsumexp(causal):
+    """With unrounded 2**x in place of the codes (mode exp2_exact) the represented
+    operator is softmax itself, so LSE_i = M_i ln 2 + ln(D_i / 6) must equal
+    log sum_j exp(z_ij) over the keys row i sees."""
+    rng = np.random.default_rng(30)
+    N, d = 256, 64
+    _, ops = _quantized_head(rng, N, d, scale_q=3.0)
+    rows = np.arange(N)
+    res = directp.forward_rows(*ops, rows, SCALE64, mode="exp2_exact", causal=causal)
+    z = _scores_natural(ops, rows, SCALE64)
+    if causal:
+        z = np.where(np.arange(N)[None, :] <= rows[:, None], z, -np.inf)
+    zmax = z.max(axis=-1, keepdims=True)
+    ref = zmax[:, 0] + np.log(np.exp(z - zmax).sum(axis=-1))
+    assert np.allclose(res["LSE"], ref, rtol=0, atol=1e-12)
+
+
+def test_causal_unrounded_reduces_to_masked_softmax_attention():
+    rng = np.random.default_rng(31)
+    N, d = 256, 64
+    _, ops = _quantized_head(rng, N, d)
+    rows = np.arange(N)
+    res = directp.forward_rows(*ops, rows, SCALE64, mode="exp2_exact", causal=True)
+    z = _scores_natural(ops, rows, SCALE64)
+    z = np.where(np.arange(N)[None, :] <= rows[:, None], z, -np.inf)
+    p = np.exp(z - z.max(axis=-1, keepdims=True))
+    v = mxfp4.scaled_operand(*ops[4:6]).T / 6.0
+    ref = (p @ v) / p.sum(axis=-1, keepdims=True)
+    assert np.allclose(res["O"], ref, rtol=0, atol=1e-12)
+
+
+def test_causal_codes_and_first_row():
+    """Hidden keys take code 0; blocks the row sees whole keep the noncausal exponent
+    and codes; row 0 sees key 0 alone, which gets code 6, so O_0 = Vhat_0 exactly."""
+    rng = np.random.default_rng(32)
+    N, d = 256, 64
+    _, ops = _quantized_head(rng, N, d)
+    rows = np.arange(N)
+    full = directp.forward_rows(*ops, rows, SCALE64)
+    cau = directp.forward_rows(*ops, rows, SCALE64, causal=True)
+    vis = np.arange(N)[None, :] <= rows[:, None]
+    assert np.all(cau["codes"][~vis] == 0)
+    whole = np.repeat((np.arange(N // 32)[None, :] * 32 + 31) <= rows[:, None], 32, axis=-1)
+    assert np.array_equal(cau["codes"][whole], full["codes"][whole])
+    blocks_whole = (np.arange(N // 32)[None, :] * 32 + 31) <= rows[:, None]
+    assert np.array_equal(cau["E"][blocks_whole], full["E"][blocks_whole])
+    assert np.all(cau["E"][(np.arange(N // 32)[None, :] * 32) > rows[:, None]] == directp.NO_BLOCK)
+    assert cau["codes"][0, 0] == 7
+    v = mxfp4.scaled_operand(*ops[4:6]).T / 6.0
+    assert np.array_equal(cau["O"][0], v[0])
+
+
+def test_direct_p_lse_stays_near_the_exact_one():
+    """The affine codes approximate 2**x, so the represented LSE stays near the exact
+    log-sum-exp.  The block maximum always takes code 6, i.e. 2**floor(y) in place of
+    2**y, so a row with one visible key (row 0) can sit up to ln 2 low; long rows
+    average the code map's error out (a plausibility band, not parity)."""
+    rng = np.random.default_rng(33)
+    N, d = 512, 128
+    _, ops = _quantized_head(rng, N, d)
+    rows = np.arange(N)
+    s = 1 / np.sqrt(d)
+    res = directp.forward_rows(*ops, rows, s, causal=True)
+    ref = directp.forward_rows(*ops, rows, s, mode="exp2_exact", causal=True)
+    dl = res["LSE"] - ref["LSE"]
+    assert np.all(dl > -np.log(2) - 1e-12) and np.all(dl < 0.25)
+    assert np.max(np.abs(dl[256:])) < 0.25 and abs(np.mean(dl[256:])) < 0.1
