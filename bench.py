@@ -82,7 +82,7 @@ def traffic_summary(fetch_csv, write_csv, out_path=TRAFFIC_FILE):
             raise SystemExit(f"expected exactly one dispatch of {key!r} in the counter file, got {hits}")
         return hits[0][0]
 
-    kname = "fwd_mxfp4_kernel<128, 8, false, false>"
+    kname = "fwd_mxfp4_kernel<128, 8, false, 0, 0>"
     copy_bytes = 256 << 20
     fs = copy_bytes / 1024 / pick(fetch, "copyBuffer")
     ws = copy_bytes / 1024 / pick(write, "copyBuffer")
@@ -273,6 +273,9 @@ def main():
     ops_anchored = fa.quantize_qkv(q, k, v, anchored=True)
     fns["guard"] = lambda: fa.forward_mxfp4(*ops_anchored, softmax_scale=w.softmax_scale, out=out,
                                             guard=GUARD_ML)
+    # the causal forward with the row normaliser saved for a backward pass
+    lse = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
+    fns["causal"] = lambda: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out, causal=True, lse=lse)
     med, _ = _time_windows(torch, fns, max(1, args.steps // 2), args.windows)
     qms, _ = _time_windows(torch, {"quant": quant_step}, 3, 3)
 
@@ -289,7 +292,7 @@ def main():
         "unit": "TFLOP/s",
         "frac": round(tflops / MXFP4_PEAK_TFLOPS, 4),
         "traffic": traffic,
-        "kernel": "fwd_mxfp4_kernel<128, 8, false, false>",
+        "kernel": "fwd_mxfp4_kernel<128, 8, false, 0, 0>",
         "measured_clock_ghz": round(clk, 3),
         "peak_at_measured_clock": round(peak_clk, 1),
         "frac_at_measured_clock": round(tflops / peak_clk, 4),
@@ -323,6 +326,10 @@ def main():
                                       "vs_affine": round(med["fp4"] / med[f"ex2_{kx}"], 3)} for kx in EX2_SWEEP},
         "guard_110_16": {"ms": round(med["guard"], 5), "tflops": round(flops / (med["guard"] * 1e-3) / 1e12, 2),
                          "vs_online": round(med["fp4"] / med["guard"], 3)},
+        # visible (query, key) pairs only: 4 d B H N (N + 1) / 2 flop
+        "causal_with_lse": {"ms": round(med["causal"], 5),
+                            "tflops": round(2.0 * w.d * w.B * w.H * w.N * (w.N + 1) / (med["causal"] * 1e-3) / 1e12, 2),
+                            "flops": "4 d B H N (N + 1) / 2"},
         "wall_ms_timed_region": round(wall_ms, 3),
         "roofline": roof,
         "gpu": torch.cuda.get_device_name(dev),

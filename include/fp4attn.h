@@ -156,6 +156,19 @@ fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_sc
  *   guard_margin        M, guard_shift  L: integers >= 0 with M + L <= 126
  *                       (Alg. 3 step 2); init 110 / 16, the paper's setting
  *                       for its 1.3B video model.
+ *   causal              1: query i sees keys j <= i only (the forward of the
+ *                       paper's causal-training route, Sec. "Pass the forward
+ *                       quantization into backward"); hidden scores take code
+ *                       0.  init 0.  Built for ex2_pairs 0, 4 and 16; not with
+ *                       the guard.
+ *   lse                 optional DEVICE pointer (NULL: not written) to
+ *                       [B, H, N] fp32: the natural-log row normaliser the
+ *                       backward reconstructs probabilities from, for the
+ *                       represented operator: LSE_i = ref_i ln 2 + ln(D_i / 6)
+ *                       where D_i is the represented denominator relative to
+ *                       2^ref_i, ref_i = M_i (online reference) or R_i + L
+ *                       (guard); exp(z_ij - LSE_i) is then the represented
+ *                       probability of key j.  init NULL.
  */
 typedef struct fp4attn_forward_options {
   uint32_t struct_size;
@@ -165,6 +178,8 @@ typedef struct fp4attn_forward_options {
   int32_t guard;
   int32_t guard_margin;
   int32_t guard_shift;
+  int32_t causal;
+  float* lse;
 } fp4attn_forward_options;
 
 /* Writes the defaults listed above (and struct_size) into *opts; NULL is ignored. */
@@ -174,9 +189,10 @@ void fp4attn_forward_options_init(fp4attn_forward_options* opts);
  * fp4attn_forward_mxfp4 with options (NULL = the defaults).  Operands, layout
  * and output as fp4attn_forward_mxfp4.  Errors: those of fp4attn_forward_mxfp4,
  * plus INVALID_ARG for a struct_size other than sizeof(fp4attn_forward_options),
- * ex2_pairs outside {0, 1, 2, 4, 8, 16}, guard not 0 or 1, or a guard margin
- * and shift outside the budget; UNSUPPORTED for the guard with ex2_pairs not
- * in {0, 4, 16}.
+ * ex2_pairs outside {0, 1, 2, 4, 8, 16}, guard or causal not 0 or 1, a guard
+ * margin and shift outside the budget, or an lse pointer that is not 16-byte
+ * aligned; UNSUPPORTED for the guard or the causal mask with ex2_pairs not in
+ * {0, 4, 16}, or both together.
  */
 fp4attn_status fp4attn_forward_mxfp4_ex(const uint8_t* q_codes, const uint8_t* q_scales,
                                         const uint8_t* k_codes, const uint8_t* k_scales,
@@ -219,7 +235,8 @@ fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t ro
  *   row_ids    [n_rows] int64, flattened (b*H + h)*N + i, STRICTLY ASCENDING
  *              (rows not found by the kernel's binary search are not dumped)
  *   p_codes    [n_rows, N/2]  the P codes fed to the PV product, nibble-packed
- *   block_exp  [n_rows, N/32] int16 absolute block exponents E_B
+ *   block_exp  [n_rows, N/32] int16 absolute block exponents E_B (-32768:
+ *              the block has no visible key under the causal mask)
  *   row_m      [n_rows] int32 final integer row reference M_i (0 under the guard)
  *   row_d      [n_rows] fp32 represented denominator relative to 2^M_i (under
  *              the guard: sum_B 2^(u'_B - 127) c_B with the published bytes)

@@ -28,7 +28,9 @@ Alg. 3 (sampled-guard) on top of Alg. 2:
    against the numerator's, so it is left out here (as in the unguarded route),
    and no quantity formed here can be subnormal for ``u'_B >= 1``.
 5. Output (eq. represented-output): ``O_i = sum_B alpha'_B sum_j q_ij (6 Vhat_j) / (6 D_i)``.
-   The common ``2**-L`` of numerator and denominator cancels.
+   The common ``2**-L`` of numerator and denominator cancels.  The saved row
+   normaliser (natural log) is ``LSE_i = (R_i + L) ln 2 + ln(D_i / 6)``: the
+   represented ``exp(z_ij)`` is ``2**(R_i + ebar_B) q_ij / 6``.
 
 The margin ``M`` and shift ``L`` are integers with ``M + L <= 126`` (Alg. 3,
 step 2), so a block at the anchor publishes a byte of at least 1.
@@ -56,7 +58,7 @@ def check_margin_shift(margin, shift):
         raise ValueError("margin M and shift L must be non-negative integers with M + L <= 126")
 
 
-def reference(raw_anchor, softmax_scale, margin):
+def anchor_reference(raw_anchor, softmax_scale, margin):
     """R_i = fp32(max_{j in anchors} fp32(raw_ij c_y) + M) for the [R, n_anchor] anchor scores."""
     c_y, _, _ = directp.fp32_coefficients(softmax_scale, 1.5, 1.2)
     y = fp32.mul(np.asarray(raw_anchor).astype(np.float32), c_y)
@@ -96,14 +98,16 @@ def block_bytes_and_codes(raw, R, softmax_scale, affine_a, affine_b, shift, ex2_
 
 
 def forward_rows(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, rows, softmax_scale,
-                 margin, shift, affine_a=1.5, affine_b=1.2, ex2_pairs=0, n_anchor=N_ANCHOR, want_codes=True):
+                 margin, shift, affine_a=1.5, affine_b=1.2, ex2_pairs=0, n_anchor=N_ANCHOR, want_codes=True,
+                 reference=None):
     """Guarded Direct-P forward for the query ``rows`` of ONE (batch, head) slice
     whose K and V are already in anchor order (the first ``n_anchor`` keys are
     the anchors).  Operands as :func:`oracle.directp.forward_rows`.
 
     Returns a dict: ``R`` [R] fp32 references, ``e``/``ebar`` [R, N/32] block and
     working exponents, ``upub`` [R, N/32] published bytes, ``D`` [R]
-    (``sum_B 2**(u'_B - 127) c_B``), ``O`` [R, d], and ``codes`` [R, N].
+    (``sum_B 2**(u'_B - 127) c_B``), ``O`` [R, d], ``LSE`` [R], and ``codes`` [R, N].
+    ``reference`` replaces the anchor-derived R_i (used by tests).
     """
     check_margin_shift(margin, shift)
     rows = np.asarray(rows, dtype=np.int64)
@@ -114,14 +118,16 @@ def forward_rows(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, rows
     if N < n_anchor:
         raise ValueError("fewer keys than anchors")
     raw = directp.raw_scores(q6, k6)
-    R = reference(raw[:, :n_anchor], softmax_scale, margin)
+    R = anchor_reference(raw[:, :n_anchor], softmax_scale, margin) if reference is None else \
+        np.asarray(reference, dtype=np.float64)
     e, ubar, upub, q, k = block_bytes_and_codes(raw, R, softmax_scale, affine_a, affine_b, shift, ex2_pairs)
     w = np.ldexp(1.0, upub.astype(np.int64) - 127)                        # alpha'_B
     nb = N // BLOCK
     D = (w * q.reshape(len(rows), nb, BLOCK).sum(axis=-1)).sum(axis=-1)   # sum_B alpha'_B c_B
     acc = (q * np.repeat(w, BLOCK, axis=-1)) @ v6
     out = {"R": R.astype(np.float64), "e": e, "ebar": ubar - 127, "upub": upub, "D": D,
-           "O": acc / (6.0 * D[:, None])}
+           "O": acc / (6.0 * D[:, None]),
+           "LSE": (R.astype(np.float64) + shift) * directp.LN_2 + np.log(D) - directp.LN_6}
     if want_codes:
         out["codes"] = k
     return out

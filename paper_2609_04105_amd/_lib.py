@@ -18,7 +18,7 @@ class ForwardOptions(ctypes.Structure):
     """fp4attn_forward_options (include/fp4attn.h)."""
     _fields_ = [("struct_size", ctypes.c_uint32), ("affine_a", ctypes.c_float), ("affine_b", ctypes.c_float),
                 ("ex2_pairs", ctypes.c_int32), ("guard", ctypes.c_int32), ("guard_margin", ctypes.c_int32),
-                ("guard_shift", ctypes.c_int32)]
+                ("guard_shift", ctypes.c_int32), ("causal", ctypes.c_int32), ("lse", ctypes.c_void_p)]
 
 
 # name -> argtypes; entry points not in RESTYPES return a status int

@@ -98,36 +98,45 @@ def _out(out, B, H, N, d, out_dtype, device):
     return out
 
 
-def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0, guard=None):
+def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0, guard=None, causal=False, lse=None):
     """An fp4attn_forward_options struct: the library's defaults, then the given
-    fields; ``guard`` = (margin, shift) turns the sampled guard on."""
+    fields; ``guard`` = (margin, shift) turns the sampled guard on; ``lse`` is a
+    contiguous fp32 GPU tensor [B, H, N] or None."""
     o = ForwardOptions()
     lib.fp4attn_forward_options_init(ctypes.byref(o))
     o.affine_a, o.affine_b, o.ex2_pairs = affine_a, affine_b, ex2_pairs
     if guard is not None:
         o.guard, (o.guard_margin, o.guard_shift) = 1, guard
+    o.causal = 1 if causal else 0
+    if lse is not None:
+        _need(lse, "lse", torch.float32, 3)
+        o.lse = lse.data_ptr()
     return o
 
 
 def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, softmax_scale=None,
-                  affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32, ex2_pairs=None, guard=None):
+                  affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32, ex2_pairs=None, guard=None,
+                  causal=False, lse=None):
     """Direct-P full-MXFP4 attention forward; returns O [B, H, N, d].
 
     ``ex2_pairs`` (0, 1, 2, 4, 8 or 16 of the 16 key pairs of each 32-key
-    block take the native exponential) or ``guard`` = (margin, shift) (the
-    sampled guard; K and V from ``quantize_qkv(..., anchored=True)``) select the
-    extended entry point; with both None the plain forward runs.
+    block take the native exponential), ``guard`` = (margin, shift) (the
+    sampled guard; K and V from ``quantize_qkv(..., anchored=True)``),
+    ``causal`` or ``lse`` (an fp32 [B, H, N] tensor that receives the row
+    normaliser) select the extended entry point; otherwise the plain forward runs.
     """
     B, H, N, d = _fp4_shape(q_codes)
     ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
     _check_operands(B, H, N, d, ops)
     out = _out(out, B, H, N, d, out_dtype, q_codes.device)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    if ex2_pairs is None and guard is None:
+    if ex2_pairs is None and guard is None and not causal and lse is None:
         check(lib.fp4attn_forward_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
                                         _DTYPES[out.dtype], _stream(out)))
     else:
-        o = forward_options(affine_a, affine_b, ex2_pairs or 0, guard)
+        if lse is not None and tuple(lse.shape) != (B, H, N):
+            raise ValueError(f"lse has shape {tuple(lse.shape)}, expected {(B, H, N)}")
+        o = forward_options(affine_a, affine_b, ex2_pairs or 0, guard, causal, lse)
         check(lib.fp4attn_forward_mxfp4_ex(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
                                            _DTYPES[out.dtype], _stream(out)))
     return out
@@ -135,7 +144,7 @@ def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, sof
 
 def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, row_ids, softmax_scale=None,
                         affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False, ex2_pairs=0,
-                        guard=None):
+                        guard=None, causal=False, lse=False):
     """Forward plus the Direct-P state of the (strictly ascending) flattened ``row_ids``.
 
     Returns a dict: out, p_codes [R, N/2] uint8, block_exp [R, N/32] int16,
@@ -159,8 +168,10 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
     }
     if wg_clock:
         res["wg_clock"] = torch.zeros((B * H * N // 128, 2), dtype=torch.int64, device=dev)
+    if lse:
+        res["lse"] = torch.empty((B, H, N), dtype=torch.float32, device=dev)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    o = forward_options(affine_a, affine_b, ex2_pairs, guard)
+    o = forward_options(affine_a, affine_b, ex2_pairs, guard, causal, res.get("lse"))
     check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
                                           _DTYPES[out_dtype], _ptr(row_ids) if R else None, R, _ptr(res["p_codes"]),
                                           _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),

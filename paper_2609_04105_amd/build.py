@@ -14,12 +14,12 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libfp4attn.so")
-SOURCES = ["fwd_mxfp4_guard.hip", "fwd_mxfp4_ex2.hip", "fwd_mxfp4.hip", "fwd_mxfp4_ex2_dense.hip", "fwd_bf16.hip",
-           "api.hip", "quantize.hip"]
+SOURCES = ["fwd_mxfp4_guard.hip", "fwd_mxfp4_causal.hip", "fwd_mxfp4_ex2.hip", "fwd_mxfp4.hip",
+           "fwd_mxfp4_ex2_dense.hip", "fwd_bf16.hip", "api.hip", "quantize.hip"]
 # The attention kernels never rely on NaN ordering in fmax; without this flag the
 # compiler canonicalizes every fmax operand with an extra v_max_f32.
 EXTRA = {f: ["-fno-honor-nans"] for f in ("fwd_mxfp4.hip", "fwd_mxfp4_ex2.hip", "fwd_mxfp4_ex2_dense.hip",
-                                          "fwd_mxfp4_guard.hip", "fwd_bf16.hip")}
+                                          "fwd_mxfp4_guard.hip", "fwd_mxfp4_causal.hip", "fwd_bf16.hip")}
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -47,7 +47,7 @@ def _compile(src):
     return obj
 
 
-def build(jobs=7, verbose=True):
+def build(jobs=8, verbose=True):
     """Compile every HIP source for gfx950 and link the shared library (always rebuilds)."""
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=jobs) as ex:
@@ -65,5 +65,5 @@ def build(jobs=7, verbose=True):
 
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
-    ap.add_argument("--jobs", type=int, default=7)
+    ap.add_argument("--jobs", type=int, default=8)
     build(ap.parse_args().jobs)

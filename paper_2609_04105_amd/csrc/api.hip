@@ -79,6 +79,8 @@ fp4attn_forward_options default_options() {
   o.guard = 0;
   o.guard_margin = 110;
   o.guard_shift = 16;
+  o.causal = 0;
+  o.lse = nullptr;
   return o;
 }
 
@@ -102,6 +104,14 @@ fp4attn_status check_options(const fp4attn_forward_options* opts, fp4attn_forwar
     if (k != 0 && k != 4 && k != 16)
       return fail(FP4ATTN_ERR_UNSUPPORTED, "the guarded forward is built for ex2_pairs 0, 4 and 16, not %d", k);
   }
+  if (opts->causal != 0 && opts->causal != 1) return fail(FP4ATTN_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if (opts->causal) {
+    if (opts->guard) return fail(FP4ATTN_ERR_UNSUPPORTED, "the causal forward has no sampled guard");
+    if (k != 0 && k != 4 && k != 16)
+      return fail(FP4ATTN_ERR_UNSUPPORTED, "the causal forward is built for ex2_pairs 0, 4 and 16, not %d", k);
+  }
+  if (opts->lse != nullptr && !aligned16(opts->lse))
+    return fail(FP4ATTN_ERR_INVALID_ARG, "lse is not 16-byte aligned");
   *out = *opts;
   return FP4ATTN_OK;
 }
@@ -111,6 +121,8 @@ void set_options(fp4attn::DirectPArgs& a, const fp4attn_forward_options& o) {
   a.guard = o.guard;
   a.guard_margin = o.guard_margin;
   a.guard_shift = o.guard_shift;
+  a.causal = o.causal;
+  a.lse = o.lse;
 }
 
 fp4attn::DirectPArgs directp_args(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,

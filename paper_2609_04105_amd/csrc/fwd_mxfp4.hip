@@ -1,48 +1,57 @@
 // Direct-P full-MXFP4 attention forward: host dispatch (the kernel and its
 // design are in fwd_mxfp4.hpp).  The EX2 = 0 variants are compiled here; the
-// native-exponential densities come from fwd_mxfp4_ex2*.hip and the guarded
-// variants from fwd_mxfp4_guard.hip, compiled in parallel with this file.
+// native-exponential densities come from fwd_mxfp4_ex2*.hip, the guarded
+// variants from fwd_mxfp4_guard.hip and the causal ones from
+// fwd_mxfp4_causal.hip, compiled in parallel with this file.
 #include "fwd_mxfp4.hpp"
 
 namespace fp4attn {
 namespace directp_detail {
 
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 0, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 1, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 2, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 8, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 0, true)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, true)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, true)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 0, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 1, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 2, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 8, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 0, kVarGuard)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, kVarGuard)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, kVarGuard)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 0, kVarCausal)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, kVarCausal)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, kVarCausal)
 
 namespace {
 
-template <int D, int NW, bool DUMP>
-hipError_t dispatch_ex2(const KParams& kp, int ex2, bool guard, hipStream_t stream) {
-  if (guard) {
-    switch (ex2) {
-      case 0: return launch_directp<D, NW, DUMP, 0, true>(kp, stream);
-      case 4: return launch_directp<D, NW, DUMP, 4, true>(kp, stream);
-      case 16: return launch_directp<D, NW, DUMP, 16, true>(kp, stream);
-      default: return hipErrorInvalidValue;
-    }
-  }
+// The guarded and causal variants exist for the densities 0, 4 and 16.
+template <int D, int NW, bool DUMP, int VAR>
+hipError_t dispatch_ex2_subset(const KParams& kp, int ex2, hipStream_t stream) {
   switch (ex2) {
-    case 0: return launch_directp<D, NW, DUMP, 0, false>(kp, stream);
-    case 1: return launch_directp<D, NW, DUMP, 1, false>(kp, stream);
-    case 2: return launch_directp<D, NW, DUMP, 2, false>(kp, stream);
-    case 4: return launch_directp<D, NW, DUMP, 4, false>(kp, stream);
-    case 8: return launch_directp<D, NW, DUMP, 8, false>(kp, stream);
-    case 16: return launch_directp<D, NW, DUMP, 16, false>(kp, stream);
+    case 0: return launch_directp<D, NW, DUMP, 0, VAR>(kp, stream);
+    case 4: return launch_directp<D, NW, DUMP, 4, VAR>(kp, stream);
+    case 16: return launch_directp<D, NW, DUMP, 16, VAR>(kp, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int D, int NW, bool DUMP>
+hipError_t dispatch_ex2(const KParams& kp, int ex2, int var, hipStream_t stream) {
+  if (var == kVarGuard) return dispatch_ex2_subset<D, NW, DUMP, kVarGuard>(kp, ex2, stream);
+  if (var == kVarCausal) return dispatch_ex2_subset<D, NW, DUMP, kVarCausal>(kp, ex2, stream);
+  switch (ex2) {
+    case 0: return launch_directp<D, NW, DUMP, 0, kVarOnline>(kp, stream);
+    case 1: return launch_directp<D, NW, DUMP, 1, kVarOnline>(kp, stream);
+    case 2: return launch_directp<D, NW, DUMP, 2, kVarOnline>(kp, stream);
+    case 4: return launch_directp<D, NW, DUMP, 4, kVarOnline>(kp, stream);
+    case 8: return launch_directp<D, NW, DUMP, 8, kVarOnline>(kp, stream);
+    case 16: return launch_directp<D, NW, DUMP, 16, kVarOnline>(kp, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int D, int NW>
-hipError_t dispatch_dump(const KParams& kp, bool dump, int ex2, bool guard, hipStream_t stream) {
-  return dump ? dispatch_ex2<D, NW, true>(kp, ex2, guard, stream) : dispatch_ex2<D, NW, false>(kp, ex2, guard, stream);
+hipError_t dispatch_dump(const KParams& kp, bool dump, int ex2, int var, hipStream_t stream) {
+  return dump ? dispatch_ex2<D, NW, true>(kp, ex2, var, stream) : dispatch_ex2<D, NW, false>(kp, ex2, var, stream);
 }
 
 }  // namespace
@@ -79,6 +88,7 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   kp.row_m = a.row_m;
   kp.row_d = a.row_d;
   kp.wg_clock = a.wg_clock;
+  kp.lse = a.lse;
   const bool dump = a.n_rows > 0;
   const int bh = a.B * a.H;
   // Eight waves (256 rows) per workgroup when that still fills the 256 CUs.
@@ -87,11 +97,10 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   kp.n_qtiles = a.N / BM;
   kp.total = kp.n_qtiles * bh;
   const int ex2 = a.ex2_pairs;
-  const bool guard = a.guard != 0;
+  const int var = a.guard ? kVarGuard : (a.causal ? kVarCausal : kVarOnline);
   if (a.d == 128)
-    return wide ? dispatch_dump<128, 8>(kp, dump, ex2, guard, stream)
-                : dispatch_dump<128, 4>(kp, dump, ex2, guard, stream);
-  return wide ? dispatch_dump<64, 8>(kp, dump, ex2, guard, stream) : dispatch_dump<64, 4>(kp, dump, ex2, guard, stream);
+    return wide ? dispatch_dump<128, 8>(kp, dump, ex2, var, stream) : dispatch_dump<128, 4>(kp, dump, ex2, var, stream);
+  return wide ? dispatch_dump<64, 8>(kp, dump, ex2, var, stream) : dispatch_dump<64, 4>(kp, dump, ex2, var, stream);
 }
 
 }  // namespace fp4attn

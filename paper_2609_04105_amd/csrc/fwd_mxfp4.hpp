@@ -29,7 +29,11 @@
 // - Native-exponential mixing (template EX2 = k of the 16 pairs of a block):
 //   selected pairs take x = fma(c_y, raw, log2 6 - E_B) through v_exp_f32 and
 //   the converter with scale 1, i.e. the ideal code Q_E2M1(2^x).
-// - Sampled guard (template GUARD, Alg. 3): the row reference is fixed from
+// - Causal variant: query i sees keys j <= i; a workgroup stops at the end of
+//   its query tile, masked scores become -inf (code 0), and query tiles are
+//   launched longest first.  Every variant can write the natural-log row
+//   normaliser of the represented operator (LSE) for a backward pass.
+// - Sampled guard (template VAR = kVarGuard, Alg. 3): the row reference is fixed from
 //   the anchor keys of the first tile instead of following the block maxima;
 //   working bytes are floored at L + 1 before the codes are formed and
 //   published shifted down by L, so no rescale branch remains.
@@ -54,6 +58,9 @@ namespace directp_detail {
 constexpr int kBN = 128;   // keys per LDS tile
 constexpr int kTau = 8;    // lazy rescale: the reference may lag the row maximum by up to 8 binades
 constexpr int kStages = 4; // LDS ring depth in tiles
+// Row-reference variants of the kernel: the online integer reference, the
+// sampled guard of Alg. 3, and the online reference with the causal mask.
+constexpr int kVarOnline = 0, kVarGuard = 1, kVarCausal = 2;
 constexpr double kLog2E = 1.4426950408889634;
 constexpr double kLog2Of6 = 2.584962500721156;
 
@@ -69,6 +76,7 @@ struct KParams {
   float c_y, c_a8, k0_8, a8, k1;
   float margin, floor_u, shift;  // sampled guard: M, L + 1, L
   int out_bf16;
+  float* lse;  // optional [B, H, N] natural-log row normaliser
   const int64_t* row_ids;
   int n_rows;
   uint8_t* p_codes;
@@ -181,8 +189,9 @@ struct TileRegs {
   }
 };
 
-template <int D, int NW, bool DUMP, int EX2, bool GUARD>
+template <int D, int NW, bool DUMP, int EX2, int VAR>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_mxfp4_kernel(const KParams p) {
+  constexpr bool GUARD = VAR == kVarGuard, CAUSAL = VAR == kVarCausal;
   static_assert(EX2 == 0 || EX2 == 1 || EX2 == 2 || EX2 == 4 || EX2 == 8 || EX2 == 16, "pairs per 32-key block");
   using L = Layout<D>;
   constexpr int BM = NW * 32;
@@ -191,8 +200,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, lr = lane & 31;
   const unsigned long long clk0 = __builtin_amdgcn_s_memtime(), rt0 = __builtin_amdgcn_s_memrealtime();
-  const int lin = xcd_remap(blockIdx.x, p.total);
-  const int bh = lin / p.n_qtiles, qt = lin % p.n_qtiles;
+  int bh, qt;
+  if constexpr (CAUSAL) {
+    // longest query tiles first, spread over the XCDs in launch order
+    const int n_bh = p.total / p.n_qtiles;
+    bh = blockIdx.x % n_bh;
+    qt = p.n_qtiles - 1 - blockIdx.x / n_bh;
+  } else {
+    const int lin = xcd_remap(blockIdx.x, p.total);
+    bh = lin / p.n_qtiles;
+    qt = lin % p.n_qtiles;
+  }
   const int N = p.N;
   const int qrow = qt * BM + wave * 32 + lr;
 
@@ -246,7 +264,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   float Mref = -1.0e6f;  // integer row reference (exact in fp32); no block seen yet
   float Rref = 0.0f;     // guard: fixed row reference from the anchor tile (Alg. 3)
 
-  const int ntiles = N / kBN;
+  const int ntiles = CAUSAL ? (qt + 1) * BM / kBN : N / kBN;  // causal: keys up to the tile's last query
   const int nsteps = 2 * ntiles;  // 64-key steps
 
   // S^T of 64-key step `sl` (0 or 1) of the tile held in `st`: two 32-key blocks.
@@ -319,7 +337,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       T = Rref + E;
     } else {
       E = floorf(m * p.c_y);
-      T = E;
+      // causal: a block with no visible key has E = -inf; a finite offset keeps
+      // its codes at 0 instead of NaN (its E8M0 byte is 0 either way)
+      T = CAUSAL ? fmaxf(E, -1.0e30f) : E;
     }
     const float c0 = fmaf(-p.a8, T, p.k0_8);    // (A (log2 6 - T) + B) / 8
     const float c1 = EX2 ? p.k1 - T : 0.0f;     // log2 6 - T, the exponent offset of 2^x
@@ -383,8 +403,23 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       if (slot >= 0) {
         const int kb = 2 * g + h;
         *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
-        p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)(int)E;
+        // -32768 marks a block with no visible key (causal mask)
+        p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)(E > -32768.0f ? (int)E : -32768);
       }
+    }
+  };
+
+  // Causal mask of 64-key step g: lane half h holds keys 64 g + 32 h + 16 t + r
+  // (register r of subtile t) for query qrow; keys after the query become -inf.
+  // Only steps that reach past the wave's first query need it (wave-uniform).
+  auto causal_mask = [&](v16f(&acc)[2], int g) {
+    if (64 * g + 63 > qt * BM + wave * 32) {
+      const int lim = qrow - (64 * g + 32 * h);  // last visible offset in this lane's block
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (16 * t + r > lim) acc[t][r] = -__builtin_inff();
     }
   };
 
@@ -434,15 +469,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     directp(SB, 0, PA, uA, std::false_type{});
   } else {
     qk(lds, std::integral_constant<int, 0>{}, SA);
+    if constexpr (CAUSAL) causal_mask(SA, 0);
     directp(SA, 0, PA, uA, std::false_type{});
     qk(lds, std::integral_constant<int, 1>{}, SA);
   }
 
   // One step of the pipeline; j is the step's position in its group of eight.
-  // GUARD: the tail group, where QK, Direct-P or the step itself may not exist.
-  auto step = [&](auto J_, auto GUARD_, int g) {
+  // TAIL: the tail group, where QK, Direct-P or the step itself may not exist.
+  auto step = [&](auto J_, auto TAIL_, int g) {
     constexpr int j = decltype(J_)::value;
-    constexpr bool guard = decltype(GUARD_)::value;
+    constexpr bool guard = decltype(TAIL_)::value;
     constexpr int sl = j % 2;                 // step within its tile
     constexpr int b_cur = (j / 2) % kStages;  // ring slot of tile t
     constexpr int b_nxt = (j / 2 + 1) % kStages;
@@ -469,16 +505,25 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       // consumer in step g+1 and serialise with the code map); emits nothing.
       asm volatile("" ::"v"(S_out[0]), "v"(S_out[1]));
     }
-    if (!guard || g + 1 < nsteps) directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
+    if (!guard || g + 1 < nsteps) {
+      // masked steps all fall in the tail group (see the loop bound below)
+      if constexpr (CAUSAL && guard) causal_mask(S_in, g + 1);
+      directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
+    }
   };
 
 
+  // The unrolled loop stops kLeft steps before the end, so that the tail group
+  // holds every step that may lack QK or Direct-P work and, with the causal
+  // mask, every step whose keys reach past a query of the tile: Direct-P of
+  // step g' >= nsteps - BM / 64 runs in step g' - 1.
+  constexpr int kLeft = CAUSAL ? BM / 64 + 1 : 2;
   int g0 = 0;
-  for (; g0 + 8 <= nsteps - 2; g0 += 8) {
+  for (; g0 + 8 <= nsteps - kLeft; g0 += 8) {
     static_for<8>([&](auto J_) { step(J_, std::false_type{}, g0 + decltype(J_)::value); });
   }
-  // tail: at most nine steps remain (nsteps - 2 - g0 < 8)
-  static_for<10>([&](auto J_) {
+  // tail: fewer than 8 + kLeft steps remain
+  static_for<8 + kLeft>([&](auto J_) {
     const int g = g0 + decltype(J_)::value;
     if (g < nsteps) step(J_, std::true_type{}, g);
   });
@@ -510,6 +555,22 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       p.row_m[slot] = GUARD ? 0 : (int)Mref;
       p.row_d[slot] = Dfin;
     }
+    if constexpr (CAUSAL) {
+      // blocks past the workgroup's last query are never visited: code 0, no exponent
+      if (slot >= 0) {
+        for (int kb = 2 * nsteps + h; kb < N / 32; kb += 2) {
+          *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = v4i{0, 0, 0, 0};
+          p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)-32768;
+        }
+      }
+    }
+  }
+  if (p.lse != nullptr && h == 0) {
+    // ln(sum_j 2^y_ij) of the represented operator: 2^ref * D / 6, with ref = M_i
+    // (online) or R_i + L (guard, whose published bytes are shifted down by L)
+    constexpr float kLn2 = 0.69314718f, kLn6 = 1.79175947f;
+    const float ref = GUARD ? Rref + p.shift : Mref;
+    p.lse[(size_t)bh * N + qrow] = ref * kLn2 + (logf(Dfin) - kLn6);
   }
   if (p.wg_clock != nullptr && tid == 0) {
     // shader-clock cycles and 100 MHz constant-clock ticks this workgroup was resident
@@ -519,27 +580,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   }
 }
 
-template <int D, int NW, bool DUMP, int EX2, bool GUARD>
+template <int D, int NW, bool DUMP, int EX2, int VAR>
 hipError_t launch_directp(const KParams& kp, hipStream_t stream) {
-  hipLaunchKernelGGL((fwd_mxfp4_kernel<D, NW, DUMP, EX2, GUARD>), dim3(kp.total), dim3(NW * 64), 0, stream, kp);
+  hipLaunchKernelGGL((fwd_mxfp4_kernel<D, NW, DUMP, EX2, VAR>), dim3(kp.total), dim3(NW * 64), 0, stream, kp);
   return hipGetLastError();
 }
 
-// Every (D, NW, DUMP) variant of one EX2 density and reference mode.
-#define FP4ATTN_DIRECTP_VARIANTS(MACRO, EX2, GUARD) \
-  MACRO(64, 4, false, EX2, GUARD)                   \
-  MACRO(64, 4, true, EX2, GUARD)                    \
-  MACRO(64, 8, false, EX2, GUARD)                   \
-  MACRO(64, 8, true, EX2, GUARD)                    \
-  MACRO(128, 4, false, EX2, GUARD)                  \
-  MACRO(128, 4, true, EX2, GUARD)                   \
-  MACRO(128, 8, false, EX2, GUARD)                  \
-  MACRO(128, 8, true, EX2, GUARD)
+// Every (D, NW, DUMP) variant of one EX2 density and reference variant.
+#define FP4ATTN_DIRECTP_VARIANTS(MACRO, EX2, VAR) \
+  MACRO(64, 4, false, EX2, VAR)                   \
+  MACRO(64, 4, true, EX2, VAR)                    \
+  MACRO(64, 8, false, EX2, VAR)                   \
+  MACRO(64, 8, true, EX2, VAR)                    \
+  MACRO(128, 4, false, EX2, VAR)                  \
+  MACRO(128, 4, true, EX2, VAR)                   \
+  MACRO(128, 8, false, EX2, VAR)                  \
+  MACRO(128, 8, true, EX2, VAR)
 
-#define FP4ATTN_DIRECTP_DECLARE(D, NW, DUMP, EX2, GUARD) \
-  extern template hipError_t launch_directp<D, NW, DUMP, EX2, GUARD>(const KParams&, hipStream_t);
-#define FP4ATTN_DIRECTP_DEFINE(D, NW, DUMP, EX2, GUARD) \
-  template hipError_t launch_directp<D, NW, DUMP, EX2, GUARD>(const KParams&, hipStream_t);
+#define FP4ATTN_DIRECTP_DECLARE(D, NW, DUMP, EX2, VAR) \
+  extern template hipError_t launch_directp<D, NW, DUMP, EX2, VAR>(const KParams&, hipStream_t);
+#define FP4ATTN_DIRECTP_DEFINE(D, NW, DUMP, EX2, VAR) \
+  template hipError_t launch_directp<D, NW, DUMP, EX2, VAR>(const KParams&, hipStream_t);
 
 }  // namespace directp_detail
 }  // namespace fp4attn

@@ -5,9 +5,9 @@
 namespace fp4attn {
 namespace directp_detail {
 
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 1, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 2, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 4, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 1, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 2, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 4, kVarOnline)
 
 }  // namespace directp_detail
 }  // namespace fp4attn

@@ -5,8 +5,8 @@
 namespace fp4attn {
 namespace directp_detail {
 
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 8, false)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 16, false)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 8, kVarOnline)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 16, kVarOnline)
 
 }  // namespace directp_detail
 }  // namespace fp4attn

@@ -6,9 +6,9 @@
 namespace fp4attn {
 namespace directp_detail {
 
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 0, true)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 4, true)
-FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 16, true)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 0, kVarGuard)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 4, kVarGuard)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DEFINE, 16, kVarGuard)
 
 }  // namespace directp_detail
 }  // namespace fp4attn

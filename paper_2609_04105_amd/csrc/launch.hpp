@@ -29,6 +29,8 @@ struct DirectPArgs {
   int ex2_pairs;  // pairs of 16 per 32-key block that take the native exponential
   int guard;      // sampled anchor reference (Alg. 3) instead of the online one
   int guard_margin, guard_shift;
+  int causal;     // query i sees keys j <= i
+  float* lse;     // optional [B, H, N] natural-log row normaliser
   // test hook (all null / zero for the plain forward)
   const int64_t* row_ids;
   int n_rows;

@@ -12,7 +12,8 @@ O_REL_L2_MAX = 2e-3        # output relative L2 error bound
 O_COS_MIN = 0.9999         # output cosine bound
 
 
-def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_codes=True, ex2_pairs=0):
+def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_codes=True, ex2_pairs=0,
+                causal=False):
     """Run the oracle on flattened query ``rows`` of fp64 arrays q, k, v [B, H, N, d].
 
     The oracle quantizes its own operands (oracle.mxfp4).  Returns a dict of
@@ -22,18 +23,18 @@ def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_c
     rows = np.asarray(rows, dtype=np.int64)
     heads = rows // N
     out = {"O": np.zeros((len(rows), d)), "E": np.zeros((len(rows), N // 32), dtype=np.int64),
-           "M": np.zeros(len(rows), dtype=np.int64), "D": np.zeros(len(rows))}
+           "M": np.zeros(len(rows), dtype=np.int64), "D": np.zeros(len(rows)), "LSE": np.zeros(len(rows))}
     if want_codes:
         out["codes"] = np.zeros((len(rows), N), dtype=np.uint8)
     for bh in np.unique(heads):
         b, h = divmod(int(bh), H)
         sel = np.nonzero(heads == bh)[0]
         local = rows[sel] % N
-        qc, qs = mxfp4.quantize(q[b, h][local], axis=-1)
+        qc, qs = mxfp4.quantize(q[b, h], axis=-1)
         kc, ks = mxfp4.quantize(k[b, h], axis=-1)
         vc, vs = mxfp4.quantize(v[b, h], axis=-2)
-        res = directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(local)), softmax_scale,
-                                   affine_a, affine_b, want_codes=want_codes, ex2_pairs=ex2_pairs)
+        res = directp.forward_rows(qc, qs, kc, ks, vc, vs, local, softmax_scale,
+                                   affine_a, affine_b, want_codes=want_codes, ex2_pairs=ex2_pairs, causal=causal)
         for key in res:
             out[key][sel] = res[key]
     return out
@@ -75,7 +76,9 @@ def check_directp_dump(dump, ref, label):
     mismatch = float(np.mean(mag != ref["codes"]))
     assert mismatch <= CODE_MISMATCH_MAX, f"{label}: code mismatch fraction {mismatch:.3e}"
     E = dump["block_exp"].cpu().numpy().astype(np.int64)
-    e_mismatch = float(np.mean(E != ref["E"]))
+    seen = ref["E"] != directp.NO_BLOCK          # blocks with a visible key (causal mask)
+    assert np.all(E[~seen] == -32768), f"{label}: a block without visible keys has an exponent"
+    e_mismatch = float(np.mean(E[seen] != ref["E"][seen]))
     assert e_mismatch <= CODE_MISMATCH_MAX, f"{label}: block exponent mismatch fraction {e_mismatch:.3e}"
     M = dump["row_m"].cpu().numpy().astype(np.int64)
     assert np.all((M <= ref["M"]) & (M >= ref["M"] - 8)), f"{label}: row reference outside [M - 8, M]"
@@ -95,7 +98,7 @@ def oracle_rows_guarded(q, k, v, rows, softmax_scale, margin, shift, ex2_pairs=0
     rows = np.asarray(rows, dtype=np.int64)
     heads = rows // N
     out = {"O": np.zeros((len(rows), d)), "ebar": np.zeros((len(rows), N // 32), dtype=np.int64),
-           "D": np.zeros(len(rows)), "codes": np.zeros((len(rows), N), dtype=np.uint8)}
+           "D": np.zeros(len(rows)), "LSE": np.zeros(len(rows)), "codes": np.zeros((len(rows), N), dtype=np.uint8)}
     for bh in np.unique(heads):
         b, h = divmod(int(bh), H)
         sel = np.nonzero(heads == bh)[0]

@@ -90,10 +90,10 @@ def test_quantize_and_bf16_validation(lib):
 def test_forward_options(lib):
     from paper_2609_04105_amd import _lib
     o = _lib.ForwardOptions()
-    assert ctypes.sizeof(o) == 28
+    assert ctypes.sizeof(o) == 40
     lib.fp4attn_forward_options_init(ctypes.byref(o))
-    assert (o.struct_size, o.affine_a, o.ex2_pairs) == (28, 1.5, 0) and abs(o.affine_b - 1.2) < 1e-6
-    assert (o.guard, o.guard_margin, o.guard_shift) == (0, 110, 16)
+    assert (o.struct_size, o.affine_a, o.ex2_pairs) == (40, 1.5, 0) and abs(o.affine_b - 1.2) < 1e-6
+    assert (o.guard, o.guard_margin, o.guard_shift, o.causal, o.lse) == (0, 110, 16, 0, None)
     e = lib.fp4attn_forward_mxfp4_ex
     for kx in (3, 5, 32, -1):
         o.ex2_pairs = kx
@@ -101,7 +101,7 @@ def test_forward_options(lib):
     o.ex2_pairs = 4
     o.struct_size = 12
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
-    o.struct_size = 28
+    o.struct_size = 40
     o.guard = 1
     for M, L in ((110, 17), (-1, 0), (0, -1)):
         o.guard_margin, o.guard_shift = M, L
@@ -112,6 +112,16 @@ def test_forward_options(lib):
     o.guard, o.ex2_pairs = 2, 4
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
     o.guard = 0
+    o.causal = 1
+    o.ex2_pairs = 2
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 2     # causal: 0, 4, 16 only
+    o.ex2_pairs, o.guard = 4, 1
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 2     # causal with guard
+    o.guard, o.causal = 0, 3
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
+    o.causal, o.lse = 0, 4096 + 4
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1     # misaligned lse
+    o.lse = None
     o.affine_a = 0.0
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
     o.affine_a = 1.5

@@ -21,20 +21,29 @@ def fa():
     return fa
 
 
-def _run_and_check(fa, host64, dev, rows, label, softmax_scale=None, affine=(1.5, 1.2), ex2_pairs=None):
+def _run_and_check(fa, host64, dev, rows, label, softmax_scale=None, affine=(1.5, 1.2), ex2_pairs=None,
+                   causal=False, lse=False):
     q, k, v = host64
     B, H, N, d = q.shape
     s = 1.0 / np.sqrt(d) if softmax_scale is None else softmax_scale
     ops = gpu_operands(*dev)
     row_ids = torch.from_numpy(np.asarray(rows, dtype=np.int64)).cuda()
-    print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)} ex2_pairs={ex2_pairs}", flush=True)
+    print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)} ex2_pairs={ex2_pairs} causal={causal}", flush=True)
     dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, affine_a=affine[0], affine_b=affine[1],
-                                  ex2_pairs=ex2_pairs or 0)
-    out = fa.forward_mxfp4(*ops, softmax_scale=s, affine_a=affine[0], affine_b=affine[1], ex2_pairs=ex2_pairs)
+                                  ex2_pairs=ex2_pairs or 0, causal=causal, lse=lse)
+    lse_out = torch.empty((B, H, N), dtype=torch.float32, device="cuda") if lse else None
+    out = fa.forward_mxfp4(*ops, softmax_scale=s, affine_a=affine[0], affine_b=affine[1], ex2_pairs=ex2_pairs,
+                           causal=causal, lse=lse_out)
     torch.cuda.synchronize()
     # the test hook runs the same kernel: identical output
     assert torch.equal(out, dump["out"]), f"{label}: debug launch output differs from the forward"
-    ref = oracle_rows(q, k, v, rows, s, *affine, ex2_pairs=ex2_pairs or 0)
+    ref = oracle_rows(q, k, v, rows, s, *affine, ex2_pairs=ex2_pairs or 0, causal=causal)
+    if lse:
+        assert torch.equal(lse_out, dump["lse"])
+        got_lse = lse_out.reshape(-1)[row_ids].cpu().numpy().astype(np.float64)
+        err = np.abs(got_lse - ref["LSE"])
+        print(f"[{label}] LSE max abs error {err.max():.2e}", flush=True)
+        assert np.all(err <= 1e-4 + 1e-6 * np.abs(ref["LSE"])), f"{label}: LSE error {err.max()}" 
     mismatch = check_directp_dump(dump, ref, label)
     got = out.reshape(-1, d)[torch.from_numpy(np.asarray(rows)).cuda()].cpu().numpy()
     rel, cos = rel_l2_cos(got, ref["O"])
@@ -302,3 +311,68 @@ def test_guard_fidelity_against_exact_attention(fa):
         print(f"[fidelity] guard M={ml[0]} L={ml[1]}: cos {cos:.6f} rel-L2 {rel[ml]:.6f} RMSE {rmse:.6f}", flush=True)
     print(f"[fidelity] online reference: rel-L2 {rel['online']:.6f}", flush=True)
     assert abs(rel[(8, 0)] / rel["online"] - 1) < 0.05
+
+
+
+# ---- causal forward and the saved row normaliser ------------------------------------------
+
+@pytest.mark.parametrize("ex2_pairs", [0, 4, 16])
+def test_causal_small_all_rows(fa, ex2_pairs):
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    _run_and_check(fa, host64, dev, workloads.sampled_rows("small_b1h8_n1024_d64"), f"causal small ex2={ex2_pairs}",
+                   ex2_pairs=ex2_pairs, causal=True, lse=True)
+
+
+@pytest.mark.parametrize("N,d,H", [(128, 64, 1), (384, 128, 2), (1152, 128, 2), (512, 128, 128)])
+def test_causal_tiles_all_rows(fa, N, d, H):
+    """One key tile, 4-wave workgroups with a partial last group, and the 8-wave launch."""
+    g = torch.Generator().manual_seed(N + d + H)
+    q, k, v = (torch.randn(1, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    rows = np.arange(H * N) if H * N <= 4096 else np.arange(0, H * N, 11)
+    _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), rows, f"causal N{N} d{d} H{H}", causal=True, lse=True)
+
+
+def test_causal_long_sampled_rows(fa):
+    name = "long_b1h32_n16384_d128"
+    host64, dev = load_workload(name)
+    _run_and_check(fa, host64, dev, workloads.sampled_rows(name), f"causal {name}", causal=True, lse=True)
+
+
+def test_lse_noncausal_and_guarded(fa):
+    host64, dev = load_workload("outlier_b2h16_n4096_d128")
+    rows = workloads.sampled_rows("outlier_b2h16_n4096_d128")
+    _run_and_check(fa, host64, dev, rows, "lse outlier", lse=True)
+    from parity import oracle_rows_guarded
+    q, k, v = host64
+    B, H, N, d = q.shape
+    ops = fa.quantize_qkv(*dev, anchored=True)
+    lse = torch.empty((B, H, N), dtype=torch.float32, device="cuda")
+    fa.forward_mxfp4(*ops, guard=(110, 16), lse=lse)
+    ref = oracle_rows_guarded(q, k, v, rows, 1 / np.sqrt(d), 110, 16)
+    err = np.abs(lse.reshape(-1)[torch.from_numpy(rows).cuda()].cpu().numpy() - ref["LSE"])
+    print(f"[lse guard] max abs error {err.max():.2e}", flush=True)
+    assert np.all(err <= 1e-4 + 1e-6 * np.abs(ref["LSE"]))
+
+
+def test_causal_first_rows_see_only_their_prefix(fa):
+    """Row 0 attends to key 0 alone: O_0 is V_0's represented value (up to the
+    epilogue's fp32 division), and changing keys after a row leaves that row's
+    output bit-identical."""
+    g = torch.Generator().manual_seed(5)
+    q, k, v = (torch.randn(1, 1, 512, 64, generator=g).to(torch.bfloat16) for _ in range(3))
+    ops = gpu_operands(q.cuda(), k.cuda(), v.cuda())
+    o1 = fa.forward_mxfp4(*ops, causal=True)
+    k2, v2 = k.clone(), v.clone()
+    k2[:, :, 300:] = torch.randn(1, 1, 212, 64, generator=g).to(torch.bfloat16)
+    v2[:, :, 300:] = torch.randn(1, 1, 212, 64, generator=g).to(torch.bfloat16)
+    ops2 = gpu_operands(q.cuda(), k2.cuda(), v2.cuda())
+    o2 = fa.forward_mxfp4(*ops2, causal=True)
+    torch.cuda.synchronize()
+    # keys 300.. share V blocks with keys 288..299 (blocks of 32 along the sequence), so rows
+    # below 288 are untouched
+    assert torch.equal(o1[:, :, :288], o2[:, :, :288])
+    from oracle import mxfp4
+    vc, vs = mxfp4.quantize(workloads.as_f64(v)[0, 0], axis=-2)
+    v_hat = mxfp4.scaled_operand(vc, vs).T[0] / 6.0
+    np.testing.assert_allclose(o1[0, 0, 0].cpu().numpy().astype(np.float64), v_hat, rtol=3e-7, atol=0)

@@ -62,7 +62,7 @@ def test_integer_reference_reduces_to_the_unguarded_codes(ex2_pairs):
 def test_codes_invariant_under_integer_shift_of_the_reference():
     _, ops = _head(3)
     raw = _raw(ops, np.arange(32))
-    R = guard.reference(raw[:, :128], S128, margin=20)
+    R = guard.anchor_reference(raw[:, :128], S128, margin=20)
     e0, _, _, _, k0 = guard.block_bytes_and_codes(raw, R, S128, 1.5, 1.2, shift=4)
     e1, _, _, _, k1 = guard.block_bytes_and_codes(raw, R + 7.0, S128, 1.5, 1.2, shift=4)
     assert np.array_equal(k0, k1) and np.array_equal(e0 - 7, e1)
@@ -92,7 +92,7 @@ def test_floored_blocks_are_never_amplified():
     rows = np.arange(64)
     raw = _raw(ops, rows)
     M, L = 30, 90
-    R = guard.reference(raw[:, :128], S128, M)
+    R = guard.anchor_reference(raw[:, :128], S128, M)
     e, ubar, upub, q, _ = guard.block_bytes_and_codes(raw, R, S128, 1.5, 1.2, L, ex2_pairs=16)
     u = np.clip(e + 127, 0, 254)
     assert np.any(u <= L - 3), "the input must put some blocks well below the floor"
@@ -161,3 +161,18 @@ def test_wan_margin_floors_sub_anchor_blocks_on_flat_rows():
     res = guard.forward_rows(*ops, rows, S128, margin=110, shift=16, want_codes=False)
     assert np.all(res["ebar"] >= -110)
     assert exact.error_metrics(res["O"], ref)[1] > 1.5 * plain
+
+
+def test_lse_matches_the_online_route_under_an_integral_reference():
+    """With an integral reference and no floor in play the guarded operator is the
+    online one (same codes, bytes shifted by R - M + L), so its normaliser
+    (R + L) ln 2 + ln(D / 6) equals the online M ln 2 + ln(D / 6)."""
+    _, ops = _head(8)
+    rows = np.arange(0, 512, 5)
+    online = directp.forward_rows(*ops, rows, S128)
+    R = online["M"].astype(np.float64) + 3.0
+    res = guard.forward_rows(*ops, rows, S128, margin=0, shift=9, reference=R)
+    assert np.all(res["ebar"] + 127 > 10)
+    assert np.array_equal(res["codes"], online["codes"])
+    assert np.allclose(res["LSE"], online["LSE"], rtol=0, atol=1e-12)
+    assert np.allclose(res["O"], online["O"], rtol=1e-13, atol=1e-15)
