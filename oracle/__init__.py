@@ -22,6 +22,9 @@ directp  Direct-P attention (Sec. "Direct-P", Fix 1 and Fix 2, Alg. 2,
          represented-output), brute-force and online (tiled) forms.
 guard    the sampled QK guard of Alg. 3 (Sec. "Fix 3"): anchor permutation,
          margin M, stored-scale shift L and the floored working byte.
+fp8pv    MXFP4 QK with FP8 (E4M3) P and V, the paper's accuracy control and
+         training route: MXFP8 quantizer, exponential P payload, represented
+         denominator.
 exact    textbook softmax attention (eq. attention-intro / exact-attention)
          and the online-softmax recurrence (eq. online-recurrence).
 prange   the probability-format range diagnostic of Table p-range
