@@ -273,6 +273,9 @@ def main():
     ops_anchored = fa.quantize_qkv(q, k, v, anchored=True)
     fns["guard"] = lambda: fa.forward_mxfp4(*ops_anchored, softmax_scale=w.softmax_scale, out=out,
                                             guard=GUARD_ML)
+    # FP8 (E4M3) P and V: the paper's accuracy control and training route
+    ops8 = fa.quantize_qkv(q, k, v, pv_fp8=True)
+    fns["fp8pv"] = lambda: fa.forward_mxfp4(*ops8, softmax_scale=w.softmax_scale, out=out, pv_fp8=True)
     # the causal forward with the row normaliser saved for a backward pass
     lse = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
     fns["causal"] = lambda: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out, causal=True, lse=lse)
@@ -326,6 +329,8 @@ def main():
                                       "vs_affine": round(med["fp4"] / med[f"ex2_{kx}"], 3)} for kx in EX2_SWEEP},
         "guard_110_16": {"ms": round(med["guard"], 5), "tflops": round(flops / (med["guard"] * 1e-3) / 1e12, 2),
                          "vs_online": round(med["fp4"] / med["guard"], 3)},
+        "fp8_pv": {"ms": round(med["fp8pv"], 5), "tflops": round(flops / (med["fp8pv"] * 1e-3) / 1e12, 2),
+                   "vs_mxfp4_pv": round(med["fp4"] / med["fp8pv"], 3)},
         # visible (query, key) pairs only: 4 d B H N (N + 1) / 2 flop
         "causal_with_lse": {"ms": round(med["causal"], 5),
                             "tflops": round(2.0 * w.d * w.B * w.H * w.N * (w.N + 1) / (med["causal"] * 1e-3) / 1e12, 2),

@@ -75,6 +75,25 @@ fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t ba
                                       void* stream);
 
 /*
+ * MXFP8 quantizer for the FP8 P/V route: E4M3 payload (bias 7, three mantissa
+ * bits, largest finite 448, subnormals kept) plus one E8M0 byte per 32 values
+ * along `axis`, with the layouts of fp4attn_quantize_mxfp4 but one code byte
+ * per value:
+ *
+ *   axis = 1: codes [batch, rows, cols],  scales [batch, rows, cols/32].
+ *   axis = 0: codes [batch, cols, rows] (transposed), scales [batch, cols, rows/32].
+ *
+ * The amplitude of a block is the smallest power of two 2^e with
+ * max|v| / 2^e <= 448 (no payload saturates); codes are v / 2^e rounded to the
+ * nearest E4M3 value, ties to even, sign bit 7 = the input's sign bit.  Zero
+ * block: u = 0; non-finite block: u = 255, zero codes.  The represented value
+ * is 2^(u-127) * e4m3(code).  Errors: as fp4attn_quantize_mxfp4.
+ */
+fp4attn_status fp4attn_quantize_mxfp8(const void* src, int src_dtype, int64_t batch, int64_t rows,
+                                      int64_t cols, int axis, uint8_t* codes, uint8_t* scales,
+                                      void* stream);
+
+/*
  * fp4attn_quantize_mxfp4 of the rows put in anchor order first (Sec. "Fix 3":
  * before the launch, globally distributed K/V rows move into the first key
  * tile; exact attention does not change).  Row r of the quantized matrix is
@@ -161,6 +180,15 @@ fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_sc
  *                       quantization into backward"); hidden scores take code
  *                       0.  init 0.  Built for ex2_pairs 0, 4 and 16; not with
  *                       the guard.
+ *   pv_fp8              1: P and V are FP8 (E4M3) instead of E2M1 (the
+ *                       paper's FP8 probability/value route, its accuracy
+ *                       control and training choice).  vt_codes/vt_scales then
+ *                       come from fp4attn_quantize_mxfp8 with axis 0 (codes
+ *                       [B, H, d, N], one byte per value).  P payload of key j
+ *                       in block B: E4M3(2^(y_j - E_B + 7)), exponential on
+ *                       every key, block maximum in [128, 256); E8M0 byte
+ *                       E_B - M_i + 120; the denominator sums the same
+ *                       payloads.  init 0.  Not with the guard or ex2_pairs.
  *   lse                 optional DEVICE pointer (NULL: not written) to
  *                       [B, H, N] fp32: the natural-log row normaliser the
  *                       backward reconstructs probabilities from, for the
@@ -168,7 +196,8 @@ fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_sc
  *                       where D_i is the represented denominator relative to
  *                       2^ref_i, ref_i = M_i (online reference) or R_i + L
  *                       (guard); exp(z_ij - LSE_i) is then the represented
- *                       probability of key j.  init NULL.
+ *                       probability of key j.  (FP8 route: LSE_i = M_i ln 2 +
+ *                       ln D_i, D_i carrying the payload's 2^-7.)  init NULL.
  */
 typedef struct fp4attn_forward_options {
   uint32_t struct_size;
@@ -179,6 +208,7 @@ typedef struct fp4attn_forward_options {
   int32_t guard_margin;
   int32_t guard_shift;
   int32_t causal;
+  int32_t pv_fp8;
   float* lse;
 } fp4attn_forward_options;
 
@@ -192,7 +222,7 @@ void fp4attn_forward_options_init(fp4attn_forward_options* opts);
  * ex2_pairs outside {0, 1, 2, 4, 8, 16}, guard or causal not 0 or 1, a guard
  * margin and shift outside the budget, or an lse pointer that is not 16-byte
  * aligned; UNSUPPORTED for the guard or the causal mask with ex2_pairs not in
- * {0, 4, 16}, or both together.
+ * {0, 4, 16}, or both together, and for pv_fp8 with the guard or ex2_pairs.
  */
 fp4attn_status fp4attn_forward_mxfp4_ex(const uint8_t* q_codes, const uint8_t* q_scales,
                                         const uint8_t* k_codes, const uint8_t* k_scales,
@@ -235,6 +265,7 @@ fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t ro
  *   row_ids    [n_rows] int64, flattened (b*H + h)*N + i, STRICTLY ASCENDING
  *              (rows not found by the kernel's binary search are not dumped)
  *   p_codes    [n_rows, N/2]  the P codes fed to the PV product, nibble-packed
+ *              ([n_rows, N] E4M3 bytes with pv_fp8)
  *   block_exp  [n_rows, N/32] int16 absolute block exponents E_B (-32768:
  *              the block has no visible key under the causal mask)
  *   row_m      [n_rows] int32 final integer row reference M_i (0 under the guard)

@@ -18,7 +18,9 @@ from .api import (  # noqa: F401
     debug_directp_mxfp4,
     forward_bf16,
     forward_mxfp4,
+    forward_options,
     quantize_mxfp4,
+    quantize_mxfp8,
     quantize_qkv,
     transpose_bf16,
 )

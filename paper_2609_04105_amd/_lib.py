@@ -18,12 +18,14 @@ class ForwardOptions(ctypes.Structure):
     """fp4attn_forward_options (include/fp4attn.h)."""
     _fields_ = [("struct_size", ctypes.c_uint32), ("affine_a", ctypes.c_float), ("affine_b", ctypes.c_float),
                 ("ex2_pairs", ctypes.c_int32), ("guard", ctypes.c_int32), ("guard_margin", ctypes.c_int32),
-                ("guard_shift", ctypes.c_int32), ("causal", ctypes.c_int32), ("lse", ctypes.c_void_p)]
+                ("guard_shift", ctypes.c_int32), ("causal", ctypes.c_int32), ("pv_fp8", ctypes.c_int32),
+                ("lse", ctypes.c_void_p)]
 
 
 # name -> argtypes; entry points not in RESTYPES return a status int
 SIGNATURES = {
     "fp4attn_quantize_mxfp4": [_c_p, _int, _i64, _i64, _i64, _int, _c_p, _c_p, _c_p],
+    "fp4attn_quantize_mxfp8": [_c_p, _int, _i64, _i64, _i64, _int, _c_p, _c_p, _c_p],
     "fp4attn_quantize_mxfp4_anchored": [_c_p, _int, _i64, _i64, _i64, _int, _i64, _c_p, _c_p, _c_p],
     "fp4attn_forward_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32] * 3 + [_c_p, _int, _c_p],
     "fp4attn_forward_bf16": [_c_p] * 3 + [_i64] * 4 + [_f32, _c_p, _int, _c_p],

@@ -63,13 +63,41 @@ def quantize_mxfp4(x, axis=-1, n_anchor=0):
     return codes, scales
 
 
-def quantize_qkv(q, k, v, anchored=False):
-    """MXFP4 operands of the forward: Q, K along d; V along the sequence (transposed).
-    ``anchored``: K and V in the anchor key order of the guarded forward (128 anchors)."""
+def quantize_mxfp8(x, axis=-1):
+    """MXFP8 (E4M3 + E8M0 per 32) codes and scales of ``x`` [..., rows, cols], one
+    code byte per value; axis as :func:`quantize_mxfp4`."""
+    _need(x, "x", (torch.float32, torch.bfloat16))
+    if x.dim() < 2:
+        raise ValueError("x needs at least two dimensions")
+    lead = tuple(x.shape[:-2])
+    rows, cols = x.shape[-2:]
+    batch = math.prod(lead) if lead else 1
+    if axis in (-1, x.dim() - 1):
+        c_axis, cshape, sshape = 1, lead + (rows, cols), lead + (rows, cols // 32)
+    elif axis in (-2, x.dim() - 2):
+        c_axis, cshape, sshape = 0, lead + (cols, rows), lead + (cols, rows // 32)
+    else:
+        raise ValueError("axis must be -1 or -2")
+    codes = torch.empty(cshape, dtype=torch.uint8, device=x.device)
+    scales = torch.empty(sshape, dtype=torch.uint8, device=x.device)
+    check(lib.fp4attn_quantize_mxfp8(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, _ptr(codes),
+                                     _ptr(scales), _stream(x)))
+    return codes, scales
+
+
+def quantize_qkv(q, k, v, anchored=False, pv_fp8=False):
+    """Operands of the forward: MXFP4 Q, K along d; V along the sequence
+    (transposed), MXFP4 or, with ``pv_fp8``, MXFP8.  ``anchored``: K and V in the
+    anchor key order of the guarded forward (128 anchors)."""
     n_anchor = 128 if anchored else 0
     qc, qs = quantize_mxfp4(q, axis=-1)
     kc, ks = quantize_mxfp4(k, axis=-1, n_anchor=n_anchor)
-    vc, vs = quantize_mxfp4(v, axis=-2, n_anchor=n_anchor)
+    if pv_fp8:
+        if anchored:
+            raise ValueError("the FP8 P/V route has no anchored form")
+        vc, vs = quantize_mxfp8(v, axis=-2)
+    else:
+        vc, vs = quantize_mxfp4(v, axis=-2, n_anchor=n_anchor)
     return qc, qs, kc, ks, vc, vs
 
 
@@ -79,10 +107,10 @@ def _fp4_shape(q_codes):
     return B, H, N, 2 * half_d
 
 
-def _check_operands(B, H, N, d, ops):
+def _check_operands(B, H, N, d, ops, pv_fp8=False):
     names = ("q_codes", "q_scales", "k_codes", "k_scales", "vt_codes", "vt_scales")
     shapes = ((B, H, N, d // 2), (B, H, N, d // 32), (B, H, N, d // 2), (B, H, N, d // 32),
-              (B, H, d, N // 2), (B, H, d, N // 32))
+              (B, H, d, N if pv_fp8 else N // 2), (B, H, d, N // 32))
     for t, name, shape in zip(ops, names, shapes):
         _need(t, name, torch.uint8, 4)
         if tuple(t.shape) != shape:
@@ -98,7 +126,7 @@ def _out(out, B, H, N, d, out_dtype, device):
     return out
 
 
-def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0, guard=None, causal=False, lse=None):
+def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0, guard=None, causal=False, lse=None, pv_fp8=False):
     """An fp4attn_forward_options struct: the library's defaults, then the given
     fields; ``guard`` = (margin, shift) turns the sampled guard on; ``lse`` is a
     contiguous fp32 GPU tensor [B, H, N] or None."""
@@ -108,6 +136,7 @@ def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0, guard=None, causal=
     if guard is not None:
         o.guard, (o.guard_margin, o.guard_shift) = 1, guard
     o.causal = 1 if causal else 0
+    o.pv_fp8 = 1 if pv_fp8 else 0
     if lse is not None:
         _need(lse, "lse", torch.float32, 3)
         o.lse = lse.data_ptr()
@@ -116,27 +145,28 @@ def forward_options(affine_a=1.5, affine_b=1.2, ex2_pairs=0, guard=None, causal=
 
 def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, softmax_scale=None,
                   affine_a=1.5, affine_b=1.2, out=None, out_dtype=torch.float32, ex2_pairs=None, guard=None,
-                  causal=False, lse=None):
+                  causal=False, lse=None, pv_fp8=False):
     """Direct-P full-MXFP4 attention forward; returns O [B, H, N, d].
 
     ``ex2_pairs`` (0, 1, 2, 4, 8 or 16 of the 16 key pairs of each 32-key
     block take the native exponential), ``guard`` = (margin, shift) (the
     sampled guard; K and V from ``quantize_qkv(..., anchored=True)``),
-    ``causal`` or ``lse`` (an fp32 [B, H, N] tensor that receives the row
-    normaliser) select the extended entry point; otherwise the plain forward runs.
+    ``causal``, ``lse`` (an fp32 [B, H, N] tensor that receives the row
+    normaliser) or ``pv_fp8`` (FP8 P and V; V from ``quantize_qkv(..., pv_fp8=True)``)
+    select the extended entry point; otherwise the plain forward runs.
     """
     B, H, N, d = _fp4_shape(q_codes)
     ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
-    _check_operands(B, H, N, d, ops)
+    _check_operands(B, H, N, d, ops, pv_fp8)
     out = _out(out, B, H, N, d, out_dtype, q_codes.device)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    if ex2_pairs is None and guard is None and not causal and lse is None:
+    if ex2_pairs is None and guard is None and not causal and lse is None and not pv_fp8:
         check(lib.fp4attn_forward_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
                                         _DTYPES[out.dtype], _stream(out)))
     else:
         if lse is not None and tuple(lse.shape) != (B, H, N):
             raise ValueError(f"lse has shape {tuple(lse.shape)}, expected {(B, H, N)}")
-        o = forward_options(affine_a, affine_b, ex2_pairs or 0, guard, causal, lse)
+        o = forward_options(affine_a, affine_b, ex2_pairs or 0, guard, causal, lse, pv_fp8)
         check(lib.fp4attn_forward_mxfp4_ex(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
                                            _DTYPES[out.dtype], _stream(out)))
     return out
@@ -144,24 +174,25 @@ def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, sof
 
 def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, row_ids, softmax_scale=None,
                         affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False, ex2_pairs=0,
-                        guard=None, causal=False, lse=False):
+                        guard=None, causal=False, lse=False, pv_fp8=False):
     """Forward plus the Direct-P state of the (strictly ascending) flattened ``row_ids``.
 
-    Returns a dict: out, p_codes [R, N/2] uint8, block_exp [R, N/32] int16,
-    row_m [R] int32, row_d [R] fp32, and with ``wg_clock`` also wg_clock
+    Returns a dict: out, p_codes [R, N/2] uint8 ([R, N] E4M3 bytes with
+    ``pv_fp8``), block_exp [R, N/32] int16, row_m [R] int32, row_d [R] fp32,
+    with ``lse`` also lse [B, H, N], and with ``wg_clock`` also wg_clock
     [B*H*N/128, 2] int64 (per workgroup: shader-clock cycles, 100 MHz ticks;
     rows past the launch's workgroup count stay zero).
     """
     B, H, N, d = _fp4_shape(q_codes)
     ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
-    _check_operands(B, H, N, d, ops)
+    _check_operands(B, H, N, d, ops, pv_fp8)
     _need(row_ids, "row_ids", torch.int64, 1)
     R = row_ids.numel()   # 0: no dump, the launch is the plain forward kernel
     dev = q_codes.device
     out = torch.empty((B, H, N, d), dtype=out_dtype, device=dev)
     res = {
         "out": out,
-        "p_codes": torch.empty((R, N // 2), dtype=torch.uint8, device=dev),
+        "p_codes": torch.empty((R, N if pv_fp8 else N // 2), dtype=torch.uint8, device=dev),
         "block_exp": torch.empty((R, N // 32), dtype=torch.int16, device=dev),
         "row_m": torch.empty((R,), dtype=torch.int32, device=dev),
         "row_d": torch.empty((R,), dtype=torch.float32, device=dev),
@@ -171,7 +202,7 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
     if lse:
         res["lse"] = torch.empty((B, H, N), dtype=torch.float32, device=dev)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    o = forward_options(affine_a, affine_b, ex2_pairs, guard, causal, res.get("lse"))
+    o = forward_options(affine_a, affine_b, ex2_pairs, guard, causal, res.get("lse"), pv_fp8)
     check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
                                           _DTYPES[out_dtype], _ptr(row_ids) if R else None, R, _ptr(res["p_codes"]),
                                           _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),

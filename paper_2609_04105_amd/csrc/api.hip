@@ -80,6 +80,7 @@ fp4attn_forward_options default_options() {
   o.guard_margin = 110;
   o.guard_shift = 16;
   o.causal = 0;
+  o.pv_fp8 = 0;
   o.lse = nullptr;
   return o;
 }
@@ -110,6 +111,9 @@ fp4attn_status check_options(const fp4attn_forward_options* opts, fp4attn_forwar
     if (k != 0 && k != 4 && k != 16)
       return fail(FP4ATTN_ERR_UNSUPPORTED, "the causal forward is built for ex2_pairs 0, 4 and 16, not %d", k);
   }
+  if (opts->pv_fp8 != 0 && opts->pv_fp8 != 1) return fail(FP4ATTN_ERR_INVALID_ARG, "pv_fp8 must be 0 or 1");
+  if (opts->pv_fp8 && (opts->guard || k != 0))
+    return fail(FP4ATTN_ERR_UNSUPPORTED, "the FP8 P/V route takes neither the guard nor ex2_pairs");
   if (opts->lse != nullptr && !aligned16(opts->lse))
     return fail(FP4ATTN_ERR_INVALID_ARG, "lse is not 16-byte aligned");
   *out = *opts;
@@ -122,6 +126,7 @@ void set_options(fp4attn::DirectPArgs& a, const fp4attn_forward_options& o) {
   a.guard_margin = o.guard_margin;
   a.guard_shift = o.guard_shift;
   a.causal = o.causal;
+  a.pv_fp8 = o.pv_fp8;
   a.lse = o.lse;
 }
 
@@ -149,7 +154,7 @@ fp4attn::DirectPArgs directp_args(const uint8_t* q_codes, const uint8_t* q_scale
 }
 
 fp4attn_status quantize_common(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
-                               int64_t n_anchor, uint8_t* codes, uint8_t* scales, void* stream) {
+                               int64_t n_anchor, uint8_t* codes, uint8_t* scales, void* stream, bool fp8 = false) {
   REQUIRE_PTR(src);
   REQUIRE_PTR(codes);
   REQUIRE_PTR(scales);
@@ -164,6 +169,10 @@ fp4attn_status quantize_common(const void* src, int src_dtype, int64_t batch, in
     return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large");
   if ((batch * other * (blocked / 32) + 255) / 256 > 0x7fffffff)
     return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large for one launch");
+  if (fp8)
+    return from_hip(fp4attn::launch_quantize_mxfp8(src, src_dtype, batch, rows, cols, axis, codes, scales,
+                                                   static_cast<hipStream_t>(stream)),
+                    "quantize launch");
   return from_hip(fp4attn::launch_quantize_mxfp4(src, src_dtype, batch, rows, cols, axis, n_anchor, codes, scales,
                                                  static_cast<hipStream_t>(stream)),
                   "quantize launch");
@@ -176,6 +185,11 @@ extern "C" {
 fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols,
                                       int axis, uint8_t* codes, uint8_t* scales, void* stream) {
   return quantize_common(src, src_dtype, batch, rows, cols, axis, 0, codes, scales, stream);
+}
+
+fp4attn_status fp4attn_quantize_mxfp8(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols,
+                                      int axis, uint8_t* codes, uint8_t* scales, void* stream) {
+  return quantize_common(src, src_dtype, batch, rows, cols, axis, 0, codes, scales, stream, true);
 }
 
 fp4attn_status fp4attn_quantize_mxfp4_anchored(const void* src, int src_dtype, int64_t batch, int64_t rows,
@@ -302,6 +316,6 @@ const char* fp4attn_status_string(int status) {
 
 const char* fp4attn_last_error(void) { return g_last_error; }
 
-int fp4attn_abi_version(void) { return (1 << 16) | 2; }
+int fp4attn_abi_version(void) { return (1 << 16) | 3; }
 
 }  // extern "C"

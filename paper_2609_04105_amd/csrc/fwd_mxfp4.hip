@@ -2,7 +2,8 @@
 // design are in fwd_mxfp4.hpp).  The EX2 = 0 variants are compiled here; the
 // native-exponential densities come from fwd_mxfp4_ex2*.hip, the guarded
 // variants from fwd_mxfp4_guard.hip and the causal ones from
-// fwd_mxfp4_causal.hip, compiled in parallel with this file.
+// fwd_mxfp4_causal.hip, the FP8 P/V route from fwd_mxfp4_fp8pv.hip, all
+// compiled in parallel with this file.
 #include "fwd_mxfp4.hpp"
 
 namespace fp4attn {
@@ -20,6 +21,8 @@ FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, kVarGuard)
 FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 0, kVarCausal)
 FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 4, kVarCausal)
 FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 16, kVarCausal)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 0, kVarOnline | kPV8)
+FP4ATTN_DIRECTP_VARIANTS(FP4ATTN_DIRECTP_DECLARE, 0, kVarCausal | kPV8)
 
 namespace {
 
@@ -36,6 +39,8 @@ hipError_t dispatch_ex2_subset(const KParams& kp, int ex2, hipStream_t stream) {
 
 template <int D, int NW, bool DUMP>
 hipError_t dispatch_ex2(const KParams& kp, int ex2, int var, hipStream_t stream) {
+  if (var == (kVarOnline | kPV8)) return launch_directp<D, NW, DUMP, 0, kVarOnline | kPV8>(kp, stream);
+  if (var == (kVarCausal | kPV8)) return launch_directp<D, NW, DUMP, 0, kVarCausal | kPV8>(kp, stream);
   if (var == kVarGuard) return dispatch_ex2_subset<D, NW, DUMP, kVarGuard>(kp, ex2, stream);
   if (var == kVarCausal) return dispatch_ex2_subset<D, NW, DUMP, kVarCausal>(kp, ex2, stream);
   switch (ex2) {
@@ -92,12 +97,14 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   const bool dump = a.n_rows > 0;
   const int bh = a.B * a.H;
   // Eight waves (256 rows) per workgroup when that still fills the 256 CUs.
+  // (the FP8 P/V route too: its d = 128 form spills a few registers with eight
+  // waves, but four waves leave one per SIMD, since its LDS ring takes 104 KiB)
   const bool wide = (a.N % 256 == 0) && (int64_t)(a.N / 256) * bh >= 256;
   const int BM = wide ? 256 : 128;
   kp.n_qtiles = a.N / BM;
   kp.total = kp.n_qtiles * bh;
   const int ex2 = a.ex2_pairs;
-  const int var = a.guard ? kVarGuard : (a.causal ? kVarCausal : kVarOnline);
+  const int var = (a.guard ? kVarGuard : (a.causal ? kVarCausal : kVarOnline)) | (a.pv_fp8 ? kPV8 : 0);
   if (a.d == 128)
     return wide ? dispatch_dump<128, 8>(kp, dump, ex2, var, stream) : dispatch_dump<128, 4>(kp, dump, ex2, var, stream);
   return wide ? dispatch_dump<64, 8>(kp, dump, ex2, var, stream) : dispatch_dump<64, 4>(kp, dump, ex2, var, stream);

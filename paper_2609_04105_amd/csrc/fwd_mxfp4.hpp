@@ -49,6 +49,8 @@
 //   and share its L2 copy of that head's K/V.
 #pragma once
 
+#include <type_traits>
+
 #include "gfx950.hpp"
 #include "launch.hpp"
 
@@ -59,8 +61,9 @@ constexpr int kBN = 128;   // keys per LDS tile
 constexpr int kTau = 8;    // lazy rescale: the reference may lag the row maximum by up to 8 binades
 constexpr int kStages = 4; // LDS ring depth in tiles
 // Row-reference variants of the kernel: the online integer reference, the
-// sampled guard of Alg. 3, and the online reference with the causal mask.
-constexpr int kVarOnline = 0, kVarGuard = 1, kVarCausal = 2;
+// sampled guard of Alg. 3, and the online reference with the causal mask;
+// kPV8 added to a variant switches P and V to FP8 (E4M3) payloads.
+constexpr int kVarOnline = 0, kVarGuard = 1, kVarCausal = 2, kPV8 = 8;
 constexpr double kLog2E = 1.4426950408889634;
 constexpr double kLog2Of6 = 2.584962500721156;
 
@@ -86,11 +89,12 @@ struct KParams {
   unsigned long long* wg_clock;
 };
 
-template <int D>
+template <int D, bool PV8 = false>
 struct Layout {
   static constexpr int kCodes = (kBN / 32) * (D / 64) * 1024;  // K fragments [sub][chunk][lane][16 B]
   static constexpr int kScales = (kBN / 32) * 64 * 4;          // [sub][lane] u32
-  static constexpr int vCodes = (kBN / 64) * (D / 32) * 1024;  // V^T fragments [step][chunk][lane][16 B]
+  // V^T fragments [step][chunk][lane][16 B] (FP8: [step][chunk][lane][32 B])
+  static constexpr int vCodes = (kBN / 64) * (D / 32) * (PV8 ? 2048 : 1024);
   static constexpr int vScales = (D / 32) * 64 * 4;            // [chunk][lane] u32
   static constexpr int kOff = 0;
   static constexpr int ksOff = kOff + kCodes;
@@ -110,21 +114,22 @@ __device__ __forceinline__ int key_of_row(int sub, int m) {
 __device__ __forceinline__ int sub_of_key(int k) { return 2 * (k >> 6) + ((k >> 4) & 1); }
 __device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * ((k >> 5) & 1) + (k & 3); }
 
-template <int D, int NW>
+template <int D, int NW, bool PV8 = false>
 struct TileRegs;
 
 // Placeholder for an unused staging set.
-template <int D>
-struct TileRegs<D, 0> {
+template <int D, bool PV8>
+struct TileRegs<D, 0, PV8> {
   __device__ __forceinline__ void load(const uint8_t*, const uint8_t*, const uint8_t*, const uint8_t*, int, int, int) {}
   __device__ __forceinline__ void store(uint8_t*, int) const {}
 };
 
-template <int D, int NW>
+template <int D, int NW, bool PV8>
 struct TileRegs {
+  using L = Layout<D, PV8>;
   static constexpr int NT = NW * 64;
-  static constexpr int nK = Layout<D>::kCodes / 16;
-  static constexpr int nV = Layout<D>::vCodes / 16;
+  static constexpr int nK = L::kCodes / 16;
+  static constexpr int nV = L::vCodes / 16;
   static constexpr int KPT = (nK + NT - 1) / NT;
   static constexpr int VPT = (nV + NT - 1) / NT;
   v4i k[KPT];
@@ -148,10 +153,20 @@ struct TileRegs {
     for (int i = 0; i < VPT; ++i) {
       const int slot = tid + i * NT;
       if (nV % NT == 0 || slot < nV) {
-        const int m = slot & 63, rest = slot >> 6;
-        const int cc = rest % (D / 32), s = rest / (D / 32);
-        const int row = cc * 32 + (m & 31);
-        v[i] = *reinterpret_cast<const v4i*>(vc + (size_t)row * (N / 2) + key0 / 2 + s * 32 + (m >> 5) * 16);
+        if constexpr (PV8) {
+          // One byte per key.  The FP8 operand's k order: lane half h holds keys
+          // 16 h + [0, 16) (bytes 0-15) and 32 + 16 h + [0, 16) (bytes 16-31) of
+          // the 64-key step, while its E8M0 byte still covers keys 32 h + [0, 32).
+          const int hh = slot & 1, m = (slot >> 1) & 63, rest = slot >> 7;
+          const int cc = rest % (D / 32), s = rest / (D / 32);
+          const int row = cc * 32 + (m & 31);
+          v[i] = *reinterpret_cast<const v4i*>(vc + (size_t)row * N + key0 + s * 64 + (m >> 5) * 16 + hh * 32);
+        } else {
+          const int m = slot & 63, rest = slot >> 6;
+          const int cc = rest % (D / 32), s = rest / (D / 32);
+          const int row = cc * 32 + (m & 31);
+          v[i] = *reinterpret_cast<const v4i*>(vc + (size_t)row * (N / 2) + key0 / 2 + s * 32 + (m >> 5) * 16);
+        }
       }
     }
     if (tid < kBN) {
@@ -164,7 +179,6 @@ struct TileRegs {
   }
 
   __device__ __forceinline__ void store(uint8_t* st, int tid) const {
-    using L = Layout<D>;
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int slot = tid + i * NT;
@@ -189,11 +203,20 @@ struct TileRegs {
   }
 };
 
+// Two waves per SIMD, except where the LDS ring allows one workgroup of four
+// waves per CU only (FP8 V tiles with d = 128: 104 KiB).
+template <int D, int NW, int VAR>
+constexpr int kMinWaves = ((VAR & kPV8) && NW == 4 && D == 128) ? 1 : 2;
+
 template <int D, int NW, bool DUMP, int EX2, int VAR>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_mxfp4_kernel(const KParams p) {
-  constexpr bool GUARD = VAR == kVarGuard, CAUSAL = VAR == kVarCausal;
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kMinWaves<D, NW, VAR>, 2))) void
+fwd_mxfp4_kernel(const KParams p) {
+  constexpr bool PV8 = (VAR & kPV8) != 0;  // FP8 (E4M3) P and V payloads
+  constexpr bool GUARD = (VAR & 7) == kVarGuard, CAUSAL = (VAR & 7) == kVarCausal;
+  static_assert(!(PV8 && (GUARD || EX2 != 0)), "the FP8 route takes the exponential on every key");
+  using POp = std::conditional_t<PV8, v8i, v4i>;  // a lane's 32 P payloads
   static_assert(EX2 == 0 || EX2 == 1 || EX2 == 2 || EX2 == 4 || EX2 == 8 || EX2 == 16, "pairs per 32-key block");
-  using L = Layout<D>;
+  using L = Layout<D, (VAR & kPV8) != 0>;
   constexpr int BM = NW * 32;
   __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * L::stage];
 
@@ -216,7 +239,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 
   const uint8_t* kc = p.kc + (size_t)bh * N * (D / 2);
   const uint8_t* ks = p.ks + (size_t)bh * N * (D / 32);
-  const uint8_t* vc = p.vc + (size_t)bh * D * (N / 2);
+  const uint8_t* vc = p.vc + (size_t)bh * D * (PV8 ? N : N / 2);
   const uint8_t* vs = p.vs + (size_t)bh * D * (N / 32);
 
   // Q^T operand, resident for the whole key loop.
@@ -254,13 +277,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   // (l % 32)'s keys 32 (l / 32) .. +31.  Row 0 of this indicator matrix selects
   // K-blocks 0 and 2 (query c's 64 keys), row 1 K-blocks 1 and 3 (query c + 16),
   // so one 16x16x128 product yields every query's code sum with the P scales.
-  const int ones_word = (lane == 0 || lane == 32 || lane == 17 || lane == 49) ? 0x22222222 : 0;  // E2M1 1.0
-  const v4i ones = {ones_word, ones_word, ones_word, ones_word};
+  // FP8: the 16x16x128 form's K-blocks mix queries c and c + 16 under one
+  // scale, so the FP8 denominator is row 0 of a 32x32x64 product instead, whose
+  // indicator row 0 (lanes 0 and 32) is all ones.
+  const bool one_lane = PV8 ? (lane == 0 || lane == 32) : (lane == 0 || lane == 32 || lane == 17 || lane == 49);
+  const int ones_word = one_lane ? (PV8 ? 0x38383838 : 0x22222222) : 0;  // E4M3 / E2M1 1.0
+  POp ones;
+#pragma unroll
+  for (int i = 0; i < (PV8 ? 8 : 4); ++i) ones[i] = ones_word;
 
   v16f O[D / 32];
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) O[c] = v16f{};
-  v4f Dacc = v4f{};  // lane c < 16: register 0 = query c, register 1 = query c + 16
+  // FP4: lane c < 16, register 0 = query c, register 1 = query c + 16.
+  // FP8: lane c < 32, register 0 = query c.
+  std::conditional_t<PV8, v16f, v4f> Dacc = {};
   float Mref = -1.0e6f;  // integer row reference (exact in fp32); no block seen yet
   float Rref = 0.0f;     // guard: fixed row reference from the anchor tile (Alg. 3)
 
@@ -286,15 +317,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 
   // PV of step `s` (0 or 1) of the tile held in `st`, and the represented
   // denominator from the same P^T operand and E8M0 bytes.
-  auto pv = [&](const uint8_t* st, auto S_, const v4i& P, int u) {
+  auto pv = [&](const uint8_t* st, auto S_, const POp& P, int u) {
     constexpr int s = decltype(S_)::value;
     static_for<D / 32>([&](auto C_) {
       constexpr int c = decltype(C_)::value;
-      const v4i vf = *reinterpret_cast<const v4i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 16);
       const int vsc = reinterpret_cast<const int*>(st + L::vsOff)[c * 64 + lane];
-      O[c] = mfma_fp4_32x32x64<2 * s, 0>(vf, P, O[c], vsc, u);
+      if constexpr (PV8) {
+        const v8i vf = *reinterpret_cast<const v8i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 32);
+        O[c] = mfma_fp8_32x32x64<2 * s, 0>(vf, P, O[c], vsc, u);
+      } else {
+        const v4i vf = *reinterpret_cast<const v4i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 16);
+        O[c] = mfma_fp4_32x32x64<2 * s, 0>(vf, P, O[c], vsc, u);
+      }
     });
-    Dacc = mfma_fp4_16x16x128<0, 0>(ones, P, Dacc, 127, u);
+    if constexpr (PV8) Dacc = mfma_fp8_32x32x64<0, 0>(ones, P, Dacc, 127, u);
+    else Dacc = mfma_fp4_16x16x128<0, 0>(ones, P, Dacc, 127, u);
   };
 
   // Instruction order of one steady-state step (the region before the rescale
@@ -314,7 +351,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   // acc[1]: keys 16-31), so the block maximum, the block exponent and the codes
   // are all lane-local, and the codes land in the K64 P^T operand as they are
   // converted.  Only the rare rescale branch exchanges the two halves' exponents.
-  auto directp = [&](const v16f(&acc)[2], int g, v4i& P, int& u, auto SCHED_) {
+  auto directp = [&](const v16f(&acc)[2], int g, POp& P, int& u, auto SCHED_) {
     // 32 values in 16 three-input maxima (v_max3_f32)
     float m = fmaxf(fmaxf(acc[0][0], acc[0][1]), acc[0][2]);
 #pragma unroll
@@ -343,30 +380,66 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
     const float c0 = fmaf(-p.a8, T, p.k0_8);    // (A (log2 6 - T) + B) / 8
     const float c1 = EX2 ? p.k1 - T : 0.0f;     // log2 6 - T, the exponent offset of 2^x
-    // Code map on u / 8.  Every byte of the four words is written below; the
-    // first convert of each word takes its own input as the overwritten value.
-    unsigned w[4];
-    static_for<4>([&](auto I_) {
-      constexpr int i = decltype(I_)::value;
-      static_for<4>([&](auto W_) {
-        constexpr int wd = decltype(W_)::value;  // word wd holds keys 8 wd .. 8 wd + 7
-        const float s_lo = acc[wd / 2][8 * (wd % 2) + 2 * i], s_hi = acc[wd / 2][8 * (wd % 2) + 2 * i + 1];
-        // pair 4 wd + i of the block (keys 8 wd + 2 i and 8 wd + 2 i + 1)
-        if constexpr (EX2 != 0 && (4 * wd + i) % (16 / (EX2 ? EX2 : 1)) == 0) {
-          const float lo = __builtin_amdgcn_exp2f(fmaf(p.c_y, s_lo, c1));
-          const float hi = __builtin_amdgcn_exp2f(fmaf(p.c_y, s_hi, c1));
-          w[wd] = cvt_pk_fp4<i>(i == 0 ? as_uint(lo) : w[wd], lo, hi, 1.0f);
-        } else {
-          const float lo = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, s_lo, c0), 0.0f, 1.0f);
-          const float hi = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, s_hi, c0), 0.0f, 1.0f);
-          w[wd] = cvt_pk_fp4<i>(i == 0 ? as_uint(lo) : w[wd], lo, hi, 0.125f);
-        }
+    if constexpr (PV8) {
+      // FP8 payload: E4M3(2^(y - T + 7)) < 256 for every key (the block maximum
+      // in [128, 256)); word w holds keys 4 w .. 4 w + 3.
+      const float c7 = 7.0f - T;
+      unsigned w8[8];  // key order: words 0-3 keys 0-15 of the lane's block, 4-7 keys 16-31
+      static_for<8>([&](auto W_) {
+        constexpr int w = decltype(W_)::value;
+        constexpr int r0 = 4 * (w % 4);
+        const float e0 = __builtin_amdgcn_exp2f(fmaf(p.c_y, acc[w / 4][r0], c7));
+        const float e1 = __builtin_amdgcn_exp2f(fmaf(p.c_y, acc[w / 4][r0 + 1], c7));
+        const float e2 = __builtin_amdgcn_exp2f(fmaf(p.c_y, acc[w / 4][r0 + 2], c7));
+        const float e3 = __builtin_amdgcn_exp2f(fmaf(p.c_y, acc[w / 4][r0 + 3], c7));
+        w8[w] = cvt_pk_fp8<true>(cvt_pk_fp8<false>(as_uint(e0), e0, e1), e2, e3);
       });
-    });
-    P = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+      if constexpr (DUMP) {
+        if (slot >= 0) {
+          const v8i keyorder = {(int)w8[0], (int)w8[1], (int)w8[2], (int)w8[3],
+                                (int)w8[4], (int)w8[5], (int)w8[6], (int)w8[7]};
+          *reinterpret_cast<v8i*>(p.p_codes + (size_t)slot * N + (2 * g + h) * 32) = keyorder;
+        }
+      }
+      // Operand k order (see TileRegs::load): the lower half keeps keys 0-15 of
+      // block 0 and takes keys 0-15 of block 1; the upper half takes keys 16-31
+      // of block 0 and keeps keys 16-31 of block 1.
+#pragma unroll
+      for (int i = 0; i < 4; ++i) swap_halves(w8[i], w8[i + 4]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) P[i] = (int)w8[i];
+    } else {
+      // Code map on u / 8.  Every byte of the four words is written below; the
+      // first convert of each word takes its own input as the overwritten value.
+      unsigned w[4];
+      static_for<4>([&](auto I_) {
+        constexpr int i = decltype(I_)::value;
+        static_for<4>([&](auto W_) {
+          constexpr int wd = decltype(W_)::value;  // word wd holds keys 8 wd .. 8 wd + 7
+          const float s_lo = acc[wd / 2][8 * (wd % 2) + 2 * i], s_hi = acc[wd / 2][8 * (wd % 2) + 2 * i + 1];
+          // pair 4 wd + i of the block (keys 8 wd + 2 i and 8 wd + 2 i + 1)
+          if constexpr (EX2 != 0 && (4 * wd + i) % (16 / (EX2 ? EX2 : 1)) == 0) {
+            const float lo = __builtin_amdgcn_exp2f(fmaf(p.c_y, s_lo, c1));
+            const float hi = __builtin_amdgcn_exp2f(fmaf(p.c_y, s_hi, c1));
+            w[wd] = cvt_pk_fp4<i>(i == 0 ? as_uint(lo) : w[wd], lo, hi, 1.0f);
+          } else {
+            const float lo = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, s_lo, c0), 0.0f, 1.0f);
+            const float hi = __builtin_amdgcn_fmed3f(fmaf(p.c_a8, s_hi, c0), 0.0f, 1.0f);
+            w[wd] = cvt_pk_fp4<i>(i == 0 ? as_uint(lo) : w[wd], lo, hi, 0.125f);
+          }
+        });
+      });
+      P = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+    }
     // Keep the code map in this basic block, next to the step's matrix work,
     // instead of letting it sink below the rescale branch (emits nothing).
-    asm volatile("" ::"v"(P));
+    if constexpr (PV8) {
+      // (a 256-bit operand would not pass the host compiler's asm checks)
+      const v4i p_lo = __builtin_shufflevector(P, P, 0, 1, 2, 3), p_hi = __builtin_shufflevector(P, P, 4, 5, 6, 7);
+      asm volatile("" ::"v"(p_lo), "v"(p_hi));
+    } else {
+      asm volatile("" ::"v"(P));
+    }
     if constexpr (decltype(SCHED_)::value) schedule_step();
     if constexpr (GUARD) {
       // published byte ubar_B - L, in [1, 254 - L]
@@ -393,16 +466,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 #pragma unroll
           for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
         Dacc[0] = ldexpf(Dacc[0], sh);
-        Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
+        if constexpr (!PV8) Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
         Mref = Mn;
       }
       // E8M0 byte of this lane's block: clamp(E - M + 127, 0, 254) (E - M <= kTau).
-      u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mref + 127.0f, 0, 0u);
+      u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mref + (PV8 ? 120.0f : 127.0f), 0, 0u);
     }
     if constexpr (DUMP) {
       if (slot >= 0) {
         const int kb = 2 * g + h;
-        *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
+        if constexpr (!PV8) *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = P;
         // -32768 marks a block with no visible key (causal mask)
         p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)(E > -32768.0f ? (int)E : -32768);
       }
@@ -431,10 +504,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   // every LDS offset and register set is a compile-time constant.
   // With four waves each thread stages twice the bytes, so only one set is kept
   // and tiles are fetched two (not three) tiles ahead.
-  constexpr bool kTwoSets = NW == 8;
+  constexpr bool kTwoSets = NW == 8 && !PV8;  // FP8 V tiles double the staged bytes
   constexpr int kAhead = kTwoSets ? 3 : 2;
-  TileRegs<D, NW> st_even;
-  TileRegs<D, kTwoSets ? NW : 0> st_odd;
+  TileRegs<D, NW, PV8> st_even;
+  TileRegs<D, kTwoSets ? NW : 0, PV8> st_odd;
   st_even.load(kc, ks, vc, vs, N, 0, tid);
   st_even.store(lds, tid);
   if constexpr (kTwoSets) {
@@ -447,7 +520,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 
   // Two S^T buffers and two P operands alternate with the step parity.
   v16f SA[2], SB[2];
-  v4i PA, PB;
+  POp PA, PB;
   int uA, uB;
   if constexpr (GUARD) {
     // Anchor (Alg. 3, steps 1-2): the largest score of the first key tile, which
@@ -529,9 +602,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   });
 
   // Epilogue: O = acc / (6 D).  The denominator sits in register 0 of the lower half.
-  const float d_lo = lane_read(Dacc[0], lane & 15), d_hi = lane_read(Dacc[1], lane & 15);
-  const float Dfin = (lane & 16) ? d_hi : d_lo;  // query lane % 32
-  const float inv = 1.0f / (6.0f * Dfin);
+  float Dfin;  // query lane % 32
+  if constexpr (PV8) {
+    Dfin = lane_read(Dacc[0], lane & 31);
+  } else {
+    const float d_lo = lane_read(Dacc[0], lane & 15), d_hi = lane_read(Dacc[1], lane & 15);
+    Dfin = (lane & 16) ? d_hi : d_lo;
+  }
+  // O = acc / (6 D) for E2M1 payloads (P and V each carry 1/6); FP8 payloads carry none
+  const float inv = 1.0f / ((PV8 ? 1.0f : 6.0f) * Dfin);
   const size_t orow = ((size_t)bh * N + qrow) * D;
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) {
@@ -559,7 +638,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       // blocks past the workgroup's last query are never visited: code 0, no exponent
       if (slot >= 0) {
         for (int kb = 2 * nsteps + h; kb < N / 32; kb += 2) {
-          *reinterpret_cast<v4i*>(p.p_codes + (size_t)slot * (N / 2) + kb * 16) = v4i{0, 0, 0, 0};
+          *reinterpret_cast<POp*>(p.p_codes + (size_t)slot * (PV8 ? N : N / 2) + kb * (PV8 ? 32 : 16)) = POp{};
           p.block_exp[(size_t)slot * (N / 32) + kb] = (int16_t)-32768;
         }
       }
@@ -570,7 +649,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     // (online) or R_i + L (guard, whose published bytes are shifted down by L)
     constexpr float kLn2 = 0.69314718f, kLn6 = 1.79175947f;
     const float ref = GUARD ? Rref + p.shift : Mref;
-    p.lse[(size_t)bh * N + qrow] = ref * kLn2 + (logf(Dfin) - kLn6);
+    // (FP8 route: D already carries the payload's 2^-7, and no 1/6)
+    p.lse[(size_t)bh * N + qrow] = ref * kLn2 + (PV8 ? logf(Dfin) : logf(Dfin) - kLn6);
   }
   if (p.wg_clock != nullptr && tid == 0) {
     // shader-clock cycles and 100 MHz constant-clock ticks this workgroup was resident

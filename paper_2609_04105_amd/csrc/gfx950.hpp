@@ -17,6 +17,11 @@
 //    becomes {E2M1(b / scale), E2M1(a / scale)} (a in the low nibble), rounding
 //    to nearest even and saturating at 6.
 //  v_permlane32_swap(a, b): a's lanes 32..63 and b's lanes 0..31 trade values.
+//  v_mfma_scale_f32_32x32x64_f8f6f4 / 16x16x128 with FP8 (E4M3) A and B: the
+//    same lane/row/k assignment with one byte per element (32 bytes per lane).
+//    (Mixing FP4 with FP8 changes the FP4 operand's k order; not used here.)
+//  v_cvt_scalef32_pk_fp8_f32: E4M3 by round to nearest even, subnormals kept;
+//    above the E4M3 rounding range the result is NaN, not saturated.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -53,6 +58,35 @@ __device__ __forceinline__ v4f mfma_fp4_16x16x128(v4i a, v4i b, v4f c, int scale
   v8i b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a8, b8, c, kFmtFp4, kFmtFp4, OPSEL_A, scale_a,
                                                            OPSEL_B, scale_b);
+}
+
+// E4M3 format selector of the f8f6f4 matrix instructions.
+constexpr int kFmtFp8 = 0;
+
+// D = A * B + C on the scaled FP8 (E4M3) matrix unit, 32x32x64 (A lane l: row
+// l % 32, k = 32 (l / 32) + [0, 32) as 32 bytes; B likewise by column).
+template <int OPSEL_A, int OPSEL_B>
+__device__ __forceinline__ v16f mfma_fp8_32x32x64(v8i a, v8i b, v16f c, int scale_a, int scale_b) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, kFmtFp8, kFmtFp8, OPSEL_A, scale_a, OPSEL_B,
+                                                          scale_b);
+}
+
+// D = A * B + C on the scaled FP8 (E4M3) matrix unit, 16x16x128 (A lane l: row
+// l % 16, k = 32 (l / 16) + [0, 32); B likewise by column).
+template <int OPSEL_A, int OPSEL_B>
+__device__ __forceinline__ v4f mfma_fp8_16x16x128(v8i a, v8i b, v4f c, int scale_a, int scale_b) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, kFmtFp8, kFmtFp8, OPSEL_A, scale_a, OPSEL_B,
+                                                           scale_b);
+}
+
+// Two fp32 values -> two E4M3 bytes (RNE; inputs must stay below the E4M3
+// overflow threshold, where the converter gives NaN), written into the low
+// (HI = false) or high 16 bits of `old`.
+template <bool HI>
+__device__ __forceinline__ unsigned cvt_pk_fp8(unsigned old, float lo, float hi) {
+  typedef short v2s __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(__builtin_bit_cast(v2s, old), lo, hi,
+                                                                                1.0f, HI));
 }
 
 // Value of `v` in lane `src` (any lane), through the LDS crossbar.

@@ -12,6 +12,9 @@ namespace fp4attn {
 hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
                                  int64_t n_anchor, uint8_t* codes, uint8_t* scales, hipStream_t stream);
 
+hipError_t launch_quantize_mxfp8(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
+                                 uint8_t* codes, uint8_t* scales, hipStream_t stream);
+
 hipError_t launch_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols, void* dst,
                                  hipStream_t stream);
 
@@ -30,6 +33,7 @@ struct DirectPArgs {
   int guard;      // sampled anchor reference (Alg. 3) instead of the online one
   int guard_margin, guard_shift;
   int causal;     // query i sees keys j <= i
+  int pv_fp8;     // P and V as FP8 (E4M3) payloads; V operands are MXFP8
   float* lse;     // optional [B, H, N] natural-log row normaliser
   // test hook (all null / zero for the plain forward)
   const int64_t* row_ids;

@@ -1,4 +1,4 @@
-// MXFP4 input quantizer and the bf16 transpose used by the BF16 baseline.
+// MXFP4 and MXFP8 input quantizers and the bf16 transpose used by the BF16 baseline.
 //
 // Quantizer (eq. mx-scale): per block of 32 values with absolute maximum a,
 // the E8M0 amplitude is 2^floor(log2 a) or 2^ceil(log2 a), whichever has the
@@ -123,6 +123,79 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_kernel(const T* __restrict
   scales[(b * outer + o) * nblk + blk] = (uint8_t)ubyte;
 }
 
+// MXFP8 (E4M3 payload + E8M0 per 32 values): the amplitude is the smallest
+// power of two 2^e with amax / 2^e <= 448, so no payload saturates; payloads
+// are v / 2^e (exact) rounded to nearest even by the hardware converter, which
+// keeps E4M3 subnormals.  Zero block: u = 0; non-finite block: u = 255, codes 0.
+// Codes are stored one byte per value, in the same orientation as the MXFP4
+// quantizer (axis 0: transposed).
+template <typename T, int AXIS>
+__global__ __launch_bounds__(256) void quantize_mxfp8_kernel(const T* __restrict__ src, int64_t batch, int64_t rows,
+                                                             int64_t cols, uint8_t* __restrict__ codes,
+                                                             uint8_t* __restrict__ scales) {
+  const int64_t nblk = AXIS == 1 ? cols / 32 : rows / 32;
+  const int64_t outer = AXIS == 1 ? rows : cols;
+  const int64_t total = batch * outer * nblk;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= total) return;
+  int64_t b, o, blk;
+  if (AXIS == 1) {
+    blk = t % nblk;
+    o = (t / nblk) % outer;
+    b = t / (nblk * outer);
+  } else {
+    o = t % outer;
+    blk = (t / outer) % nblk;
+    b = t / (outer * nblk);
+  }
+  float v[32];
+  if (AXIS == 1) {
+    const T* p = src + (b * rows + o) * cols + blk * 32;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + j);
+  } else {
+    const T* p = src + (b * rows + blk * 32) * cols + o;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + (int64_t)j * cols);
+  }
+  float amax = 0.0f;
+  bool finite = true;
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    finite = finite && __builtin_isfinite(v[j]);
+    amax = fmaxf(amax, fabsf(v[j]));
+  }
+  unsigned ubyte;
+  int e = 0;
+  if (!finite) {
+    ubyte = 255;
+  } else if (amax == 0.0f) {
+    ubyte = 0;
+  } else {
+    int x;
+    frexpf(amax, &x);          // amax = m 2^x, m in [0.5, 1)
+    e = x - 9;                 // amax / 2^e in [256, 512)
+    if (ldexpf(amax, -e) > 448.0f) ++e;
+    e = e < -127 ? -127 : (e > 127 ? 127 : e);
+    ubyte = (unsigned)(e + 127);
+  }
+  unsigned w[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if (finite) {
+      const float a0 = ldexpf(v[4 * i], -e), a1 = ldexpf(v[4 * i + 1], -e);
+      const float a2 = ldexpf(v[4 * i + 2], -e), a3 = ldexpf(v[4 * i + 3], -e);
+      w[i] = cvt_pk_fp8<true>(cvt_pk_fp8<false>(0u, a0, a1), a2, a3);
+    } else {
+      w[i] = 0u;
+    }
+  }
+  uint8_t* cdst = codes + (b * outer + o) * (nblk * 32) + blk * 32;
+  *reinterpret_cast<v4i*>(cdst) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  *reinterpret_cast<v4i*>(cdst + 16) = v4i{(int)w[4], (int)w[5], (int)w[6], (int)w[7]};
+  scales[(b * outer + o) * nblk + blk] = (uint8_t)ubyte;
+}
+
 // dst[b, c, r] = src[b, r, c] for bf16, through a 64 x 64 LDS tile.
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ src, int64_t rows,
                                                              int64_t cols, uint16_t* __restrict__ dst) {
@@ -163,6 +236,30 @@ hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, 
     else
       hipLaunchKernelGGL((quantize_mxfp4_kernel<uint16_t, 0>), grid, block, 0, stream, (const uint16_t*)src, batch,
                          rows, cols, codes, scales, n_anchor, stride);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_mxfp8(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
+                                 uint8_t* codes, uint8_t* scales, hipStream_t stream) {
+  const int64_t nblk = axis == 1 ? cols / 32 : rows / 32;
+  const int64_t outer = axis == 1 ? rows : cols;
+  const int64_t total = batch * outer * nblk;
+  const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  if (src_dtype == 0) {
+    if (axis == 1)
+      hipLaunchKernelGGL((quantize_mxfp8_kernel<float, 1>), grid, block, 0, stream, (const float*)src, batch, rows,
+                         cols, codes, scales);
+    else
+      hipLaunchKernelGGL((quantize_mxfp8_kernel<float, 0>), grid, block, 0, stream, (const float*)src, batch, rows,
+                         cols, codes, scales);
+  } else {
+    if (axis == 1)
+      hipLaunchKernelGGL((quantize_mxfp8_kernel<uint16_t, 1>), grid, block, 0, stream, (const uint16_t*)src, batch,
+                         rows, cols, codes, scales);
+    else
+      hipLaunchKernelGGL((quantize_mxfp8_kernel<uint16_t, 0>), grid, block, 0, stream, (const uint16_t*)src, batch,
+                         rows, cols, codes, scales);
   }
   return hipGetLastError();
 }

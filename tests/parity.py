@@ -128,3 +128,46 @@ def check_guarded_dump(dump, ref, label):
     rel = np.abs(D - ref["D"]) / ref["D"]
     assert rel.max() < 1e-4, f"{label}: denominator rel error {rel.max():.3e}"
     return mismatch
+
+
+def oracle_rows_fp8(q, k, v, rows, softmax_scale, causal=False):
+    """The FP8-P/V oracle (MXFP4 QK, E4M3 P, MXFP8 V) on flattened query ``rows``."""
+    from oracle import fp8pv
+    B, H, N, d = q.shape
+    rows = np.asarray(rows, dtype=np.int64)
+    heads = rows // N
+    out = {"O": np.zeros((len(rows), d)), "E": np.zeros((len(rows), N // 32), dtype=np.int64),
+           "M": np.zeros(len(rows), dtype=np.int64), "D": np.zeros(len(rows)), "LSE": np.zeros(len(rows)),
+           "codes": np.zeros((len(rows), N), dtype=np.uint8)}
+    for bh in np.unique(heads):
+        b, h = divmod(int(bh), H)
+        sel = np.nonzero(heads == bh)[0]
+        qc, qs = mxfp4.quantize(q[b, h], axis=-1)
+        kc, ks = mxfp4.quantize(k[b, h], axis=-1)
+        vc, vs = fp8pv.quantize(v[b, h], axis=-2)
+        res = fp8pv.forward_rows(qc, qs, kc, ks, vc, vs, rows[sel] % N, softmax_scale, causal=causal)
+        for key in out:
+            out[key][sel] = res[key]
+    return out
+
+
+def check_fp8_dump(dump, ref, label):
+    """FP8 route: E4M3 payload bytes (non-negative), block exponents, row reference
+    within the lazy window, and the denominator."""
+    codes = dump["p_codes"].cpu().numpy()
+    assert not np.any(codes & 0x80), f"{label}: a P payload carries a sign bit"
+    mismatch = float(np.mean(codes != ref["codes"]))
+    assert mismatch <= CODE_MISMATCH_MAX, f"{label}: payload mismatch fraction {mismatch:.3e}"
+    E = dump["block_exp"].cpu().numpy().astype(np.int64)
+    seen = ref["E"] != directp.NO_BLOCK
+    assert np.all(E[~seen] == -32768)
+    assert float(np.mean(E[seen] != ref["E"][seen])) <= CODE_MISMATCH_MAX
+    M = dump["row_m"].cpu().numpy().astype(np.int64)
+    assert np.all((M <= ref["M"]) & (M >= ref["M"] - 8)), f"{label}: row reference outside [M - 8, M]"
+    D = dump["row_d"].cpu().numpy().astype(np.float64) * np.exp2(M - ref["M"])
+    rel = np.abs(D - ref["D"]) / ref["D"]
+    # E4M3 payload sums are not exact in fp32 (E2M1 code sums are): the bound of
+    # recursive fp32 summation of N positive terms, N * 2^-24
+    tol = max(1e-4, codes.shape[1] * 2.0 ** -24)
+    assert rel.max() < tol, f"{label}: denominator rel error {rel.max():.3e} (bound {tol:.1e})"
+    return mismatch

@@ -72,6 +72,9 @@ def test_quantize_and_bf16_validation(lib):
     assert q(FAKE[0], 2, 1, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # dtype
     assert q(FAKE[0], 0, 1, 4, 64, 2, FAKE[1], FAKE[2], None) == 1     # axis
     assert q(FAKE[0], 0, 0, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # batch
+    q8 = lib.fp4attn_quantize_mxfp8
+    assert q8(FAKE[0], 0, 1, 4, 48, 1, FAKE[1], FAKE[2], None) == 1    # cols not /32
+    assert q8(None, 0, 1, 4, 64, 1, FAKE[1], FAKE[2], None) == 1
     qa = lib.fp4attn_quantize_mxfp4_anchored
     assert qa(FAKE[0], 0, 1, 256, 64, 1, 0, FAKE[1], FAKE[2], None) == 1     # n_anchor < 1
     assert qa(FAKE[0], 0, 1, 256, 64, 1, 96, FAKE[1], FAKE[2], None) == 1    # does not divide rows
@@ -90,10 +93,10 @@ def test_quantize_and_bf16_validation(lib):
 def test_forward_options(lib):
     from paper_2609_04105_amd import _lib
     o = _lib.ForwardOptions()
-    assert ctypes.sizeof(o) == 40
+    assert ctypes.sizeof(o) == 48
     lib.fp4attn_forward_options_init(ctypes.byref(o))
-    assert (o.struct_size, o.affine_a, o.ex2_pairs) == (40, 1.5, 0) and abs(o.affine_b - 1.2) < 1e-6
-    assert (o.guard, o.guard_margin, o.guard_shift, o.causal, o.lse) == (0, 110, 16, 0, None)
+    assert (o.struct_size, o.affine_a, o.ex2_pairs) == (48, 1.5, 0) and abs(o.affine_b - 1.2) < 1e-6
+    assert (o.guard, o.guard_margin, o.guard_shift, o.causal, o.pv_fp8, o.lse) == (0, 110, 16, 0, 0, None)
     e = lib.fp4attn_forward_mxfp4_ex
     for kx in (3, 5, 32, -1):
         o.ex2_pairs = kx
@@ -101,7 +104,7 @@ def test_forward_options(lib):
     o.ex2_pairs = 4
     o.struct_size = 12
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
-    o.struct_size = 40
+    o.struct_size = 48
     o.guard = 1
     for M, L in ((110, 17), (-1, 0), (0, -1)):
         o.guard_margin, o.guard_shift = M, L
@@ -122,6 +125,13 @@ def test_forward_options(lib):
     o.causal, o.lse = 0, 4096 + 4
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1     # misaligned lse
     o.lse = None
+    o.pv_fp8, o.ex2_pairs = 1, 4
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 2     # fp8 P/V with ex2
+    o.ex2_pairs, o.guard = 0, 1
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 2     # fp8 P/V with guard
+    o.guard, o.pv_fp8 = 0, 2
+    assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
+    o.pv_fp8, o.ex2_pairs = 0, 4
     o.affine_a = 0.0
     assert e(*FAKE[:6], 1, 1, 128, 64, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 1
     o.affine_a = 1.5

@@ -376,3 +376,76 @@ def test_causal_first_rows_see_only_their_prefix(fa):
     vc, vs = mxfp4.quantize(workloads.as_f64(v)[0, 0], axis=-2)
     v_hat = mxfp4.scaled_operand(vc, vs).T[0] / 6.0
     np.testing.assert_allclose(o1[0, 0, 0].cpu().numpy().astype(np.float64), v_hat, rtol=3e-7, atol=0)
+
+
+# ---- FP8 (E4M3) P and V -----------------------------------------------------------------
+
+def _run_fp8(fa, host64, dev, rows, label, causal=False):
+    from parity import check_fp8_dump, oracle_rows_fp8
+    q, k, v = host64
+    B, H, N, d = q.shape
+    s = 1.0 / np.sqrt(d)
+    ops = fa.quantize_qkv(*dev, pv_fp8=True)
+    row_ids = torch.from_numpy(np.asarray(rows, dtype=np.int64)).cuda()
+    print(f"[{label}] fp8 P/V causal={causal} B{B} H{H} N{N} d{d} rows={len(rows)}", flush=True)
+    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, pv_fp8=True, causal=causal, lse=True)
+    lse = torch.empty((B, H, N), dtype=torch.float32, device="cuda")
+    out = fa.forward_mxfp4(*ops, softmax_scale=s, pv_fp8=True, causal=causal, lse=lse)
+    torch.cuda.synchronize()
+    assert torch.equal(out, dump["out"]) and torch.equal(lse, dump["lse"])
+    ref = oracle_rows_fp8(q, k, v, rows, s, causal)
+    mismatch = check_fp8_dump(dump, ref, label)
+    got = out.reshape(-1, d)[row_ids].cpu().numpy()
+    rel, cos = rel_l2_cos(got, ref["O"])
+    err = np.abs(lse.reshape(-1)[row_ids].cpu().numpy() - ref["LSE"])
+    print(f"[{label}] payload mismatch {mismatch:.2e}  O rel-L2 {rel:.3e}  cos {cos:.8f}  LSE err {err.max():.2e}",
+          flush=True)
+    assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{label}: rel {rel} cos {cos}"
+    # ln of the denominator: the same fp32 summation bound as the denominator itself
+    assert np.all(err <= max(1e-4, N * 2.0 ** -24) + 1e-6 * np.abs(ref["LSE"]))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_fp8pv_small_all_rows(fa, causal):
+    host64, dev = load_workload("small_b1h8_n1024_d64")
+    _run_fp8(fa, host64, dev, workloads.sampled_rows("small_b1h8_n1024_d64"), "small", causal)
+
+
+@pytest.mark.parametrize("N,d,H", [(128, 64, 1), (384, 128, 2), (1152, 128, 2), (512, 128, 128)])
+def test_fp8pv_tiles(fa, N, d, H):
+    g = torch.Generator().manual_seed(N + 3 * d + H)
+    q, k, v = (torch.randn(1, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    rows = np.arange(H * N) if H * N <= 4096 else np.arange(0, H * N, 11)
+    _run_fp8(fa, host64, (q.cuda(), k.cuda(), v.cuda()), rows, f"N{N} d{d} H{H}", causal=(N == 384))
+
+
+@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "long_b1h32_n16384_d128"])
+def test_fp8pv_full_size_sampled_rows(fa, name):
+    host64, dev = load_workload(name)
+    _run_fp8(fa, host64, dev, workloads.sampled_rows(name), name)
+
+
+def test_fp8pv_fidelity_against_exact_attention(fa):
+    """FP8 P/V is the accurate route (Table accuracy-matched-control): on the long
+    workload's sampled rows its error against exact attention is well below the
+    Direct-P MXFP4 route's."""
+    from oracle import exact
+    name = "long_b1h32_n16384_d128"
+    (q, k, v), dev = load_workload(name)
+    rows = workloads.sampled_rows(name)
+    B, H, N, d = q.shape
+    s = 1.0 / np.sqrt(d)
+    ref = np.zeros((len(rows), d))
+    for bh in np.unique(rows // N):
+        sel = np.nonzero(rows // N == bh)[0]
+        b, h = divmod(int(bh), H)
+        ref[sel] = exact.attention(q[b, h][rows[sel] % N], k[b, h], v[b, h], s)
+    idx = torch.from_numpy(rows).cuda()
+    o4 = fa.forward_mxfp4(*gpu_operands(*dev)).reshape(-1, d)[idx].cpu().numpy()
+    o8 = fa.forward_mxfp4(*fa.quantize_qkv(*dev, pv_fp8=True), pv_fp8=True).reshape(-1, d)[idx].cpu().numpy()
+    m4 = exact.error_metrics(o4, ref)
+    m8 = exact.error_metrics(o8, ref)
+    print(f"[fidelity] MXFP4 P/V cos {m4[0]:.6f} rel-L2 {m4[1]:.6f}; FP8 P/V cos {m8[0]:.6f} rel-L2 {m8[1]:.6f}",
+          flush=True)
+    assert m8[0] > 0.98 and m8[1] < 0.55 * m4[1]

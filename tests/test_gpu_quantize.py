@@ -102,3 +102,51 @@ def test_anchor_order(fa, axis, rows):
     cg, sg = fa.quantize_mxfp4(x.cuda(), axis=axis, n_anchor=128)
     co, so = mxfp4.quantize(workloads.as_f64(x)[:, perm], axis=axis)
     assert np.array_equal(sg.cpu().numpy(), so) and np.array_equal(cg.cpu().numpy(), co)
+
+
+def _check8(fa, x_cpu, axis):
+    from oracle import fp8pv
+    cg, sg = fa.quantize_mxfp8(x_cpu.cuda(), axis=axis)
+    co, so = fp8pv.quantize(workloads.as_f64(x_cpu), axis=axis)
+    assert np.array_equal(sg.cpu().numpy(), so), "MXFP8 scale bytes differ"
+    assert np.array_equal(cg.cpu().numpy(), co), "MXFP8 code bytes differ"
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("axis", [-1, -2])
+def test_mxfp8_ragged_random(fa, dtype, axis):
+    g = torch.Generator().manual_seed(101)
+    x = (torch.randn(3, 96, 160, generator=g) * torch.exp2(torch.randint(-20, 20, (3, 96, 160), generator=g))).to(dtype)
+    _check8(fa, x, axis)
+
+
+@pytest.mark.parametrize("axis", [-1, -2])
+def test_mxfp8_adversarial_blocks(fa, axis):
+    """Ties of the E4M3 grid, subnormal payloads, an exact 448 maximum, values just
+    above it (the next power of two takes over), zeros, negative zero, NaN and
+    infinities."""
+    from oracle import fp8pv
+    grid = torch.tensor(fp8pv.E4M3, dtype=torch.float64)
+    mids = ((grid[1:] + grid[:-1]) / 2)[:32]
+    blocks = [
+        torch.cat([torch.tensor([448.0]), mids[:31]]),                       # ties, amplitude 2^0
+        torch.cat([torch.tensor([448.0]), grid[1:32] * 0.75]),               # subnormal payloads
+        torch.cat([torch.tensor([449.0]), -mids[:31]]),                      # just above 448
+        torch.zeros(32),
+        torch.cat([torch.tensor([-0.0, 1.0]), torch.zeros(30)]),
+        torch.cat([torch.tensor([float("nan")]), torch.ones(31)]),
+        torch.cat([torch.tensor([float("inf")]), torch.ones(31)]),
+        torch.linspace(-1e-3, 1e-3, 32),
+    ]
+    x = torch.stack(blocks).to(torch.float32).reshape(1, 8, 32).repeat(1, 4, 1)   # [1, 32 rows, 32 cols]
+    if axis == -2:
+        x = x.transpose(-1, -2).contiguous()
+    _check8(fa, x, axis)
+
+
+def test_mxfp8_workload_v(fa):
+    from oracle import fp8pv
+    q, k, v = workloads.generate("outlier_b2h16_n4096_d128")
+    cg, sg = fa.quantize_mxfp8(v.cuda(), axis=-2)
+    co, so = fp8pv.quantize(workloads.as_f64(v), axis=-2)
+    assert np.array_equal(sg.cpu().numpy(), so) and np.array_equal(cg.cpu().numpy(), co)
