@@ -98,7 +98,7 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   const int bh = a.B * a.H;
   // Eight waves (256 rows) per workgroup when that still fills the 256 CUs.
   // (the FP8 P/V route too: its d = 128 form spills a few registers with eight
-  // waves, but four waves leave one per SIMD, since its LDS ring takes 104 KiB)
+  // waves, but four waves leave one per SIMD, since its LDS ring takes 108 KiB)
   const bool wide = (a.N % 256 == 0) && (int64_t)(a.N / 256) * bh >= 256;
   const int BM = wide ? 256 : 128;
   kp.n_qtiles = a.N / BM;

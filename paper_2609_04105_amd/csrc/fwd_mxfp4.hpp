@@ -41,8 +41,8 @@
 //   constant indicator operand, so it uses exactly the codes and E8M0 bytes of
 //   PV and costs no vector-ALU work.
 // - K/V tiles of 128 keys are staged in LDS in matrix-operand order (each
-//   lane's 16-byte fragment contiguous): a ring of four tiles, filled from
-//   registers that fetch two or three tiles ahead.  The key loop is software
+//   lane's 16-byte fragment contiguous): a ring of four tiles filled three
+//   tiles ahead by direct-to-LDS loads.  The key loop is software
 //   pipelined two deep: while the vector ALU maps step g+1 to codes, the
 //   matrix unit runs PV of step g and QK of step g+2.
 // - Workgroups are remapped so that the query tiles of one head run on one XCD
@@ -100,7 +100,12 @@ struct Layout {
   static constexpr int ksOff = kOff + kCodes;
   static constexpr int vOff = ksOff + kScales;
   static constexpr int vsOff = vOff + vCodes;
-  static constexpr int stage = vsOff + vScales;
+  // E8M0 words as copied from global memory: the tile's K scales (contiguous,
+  // d / 32 bytes per key), then one word of four 32-key block scales per V^T row
+  static constexpr int rawK = kBN * (D / 32) / 4;  // words
+  static constexpr int rawV = D;
+  static constexpr int rawOff = vsOff + vScales;
+  static constexpr int stage = rawOff + 4 * (rawK + rawV);
 };
 
 // Key order of the S^T product.  Operand row m = 8 g + 4 h + i of QK subtile
@@ -114,97 +119,146 @@ __device__ __forceinline__ int key_of_row(int sub, int m) {
 __device__ __forceinline__ int sub_of_key(int k) { return 2 * (k >> 6) + ((k >> 4) & 1); }
 __device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * ((k >> 5) & 1) + (k & 3); }
 
-template <int D, int NW, bool PV8 = false>
-struct TileRegs;
+// Direct-to-LDS copies: lane l's 16 (4) bytes from `base` + `off` (a 64-bit
+// scalar base and this lane's 32-bit offset) land at LDS byte address `lds` +
+// 16 l (4 l), the LDS base being taken from M0.  Written as inline assembly so
+// that the compiler counts neither the loads nor the LDS they write (it would
+// otherwise wait for every copy in flight before each LDS read); the kernel
+// waits for its own copies with vm_wait before the barrier that publishes a
+// tile.  M0 is restored afterwards, and one wait state separates its write
+// from the load that reads it.
+__device__ __forceinline__ void lds_copy16(unsigned lds, const uint8_t* base, unsigned off) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(off), "s"(base)
+      : "memory");
+}
+__device__ __forceinline__ void lds_copy4(unsigned lds, const uint8_t* base, unsigned off) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+      "global_load_lds_dword %2, %3\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(off), "s"(base)
+      : "memory");
+}
+// Wait until at most n of this wave's vector-memory operations are in flight.
+template <int n>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
+}
+__device__ __forceinline__ unsigned lds_address(const uint8_t* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
 
-// Placeholder for an unused staging set.
-template <int D, bool PV8>
-struct TileRegs<D, 0, PV8> {
-  __device__ __forceinline__ void load(const uint8_t*, const uint8_t*, const uint8_t*, const uint8_t*, int, int, int) {}
-  __device__ __forceinline__ void store(uint8_t*, int) const {}
-};
-
+// One 128-key tile: K and V^T codes copied from global memory straight into an
+// LDS stage in operand order, and its E8M0 words copied raw, then rearranged
+// in LDS by the wave that copied them.
+//   Codes: item i is one 16-byte operand fragment, K items first, then V^T
+//   items; thread tid copies items tid, tid + NT, ...  A wave's 64 lanes copy
+//   64 consecutive fragments, the order in which the direct-to-LDS load writes.
+//   Scales: kPer raw words per wave (lane l < kPer of wave w copies word
+//   w kPer + l), so every wave issues the same number of loads per tile.
+// The per-lane source offsets do not depend on the tile; only the scalar base
+// moves with the tile's first key.
 template <int D, int NW, bool PV8>
-struct TileRegs {
+struct TileCopy {
   using L = Layout<D, PV8>;
   static constexpr int NT = NW * 64;
   static constexpr int nK = L::kCodes / 16;
   static constexpr int nV = L::vCodes / 16;
-  static constexpr int KPT = (nK + NT - 1) / NT;
-  static constexpr int VPT = (nV + NT - 1) / NT;
-  v4i k[KPT];
-  v4i v[VPT];
-  unsigned ks, vs;
+  static constexpr int kItems = nK + nV;
+  static constexpr int kPerThread = (kItems + NT - 1) / NT;
+  static constexpr int kPer = (L::rawK + L::rawV) / NW;  // raw scale words per wave
+  static constexpr int kLoads = kItems / NT + 1;          // loads every wave issues per tile, at least
+  static_assert(nK % 64 == 0 && nV % 64 == 0, "whole waves per operand");
+  static_assert(kPer * NW == L::rawK + L::rawV && kPer <= 64 && L::rawK % kPer == 0, "whole waves per scale operand");
 
-  __device__ __forceinline__ void load(const uint8_t* kc, const uint8_t* ks_, const uint8_t* vc, const uint8_t* vs_,
-                                       int N, int key0, int tid) {
+  unsigned off[kPerThread];  // this lane's byte offset from the tile's K or V^T base
+  unsigned raw_off;          // and from its K or V^T scale base
+  int wave;                  // wave-uniform
+
+  __device__ __forceinline__ void init(int N, int tid) {
+    wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nK % NT == 0 || slot < nK) {
-        const int m = slot & 63, rest = slot >> 6;
+    for (int i = 0; i < kPerThread; ++i) {
+      const int item = wave * 64 + i * NT + lane;
+      if (item < nK) {
+        const int m = item & 63, rest = item >> 6;
         const int c = rest % (D / 64), sub = rest / (D / 64);
-        const int key = key_of_row(sub, m & 31);
-        const int j = 2 * c + (m >> 5);
-        k[i] = *reinterpret_cast<const v4i*>(kc + (size_t)(key0 + key) * (D / 2) + j * 16);
+        off[i] = key_of_row(sub, m & 31) * (D / 2) + (2 * c + (m >> 5)) * 16;
+      } else if constexpr (PV8) {
+        // One byte per key.  The FP8 operand's k order: lane half h holds keys
+        // 16 h + [0, 16) (bytes 0-15) and 32 + 16 h + [0, 16) (bytes 16-31) of
+        // the 64-key step, while its E8M0 byte still covers keys 32 h + [0, 32).
+        const int vi = item - nK;
+        const int hh = vi & 1, m = (vi >> 1) & 63, rest = vi >> 7;
+        const int cc = rest % (D / 32), s = rest / (D / 32);
+        off[i] = (cc * 32 + (m & 31)) * N + s * 64 + (m >> 5) * 16 + hh * 32;
+      } else {
+        const int vi = item - nK;
+        const int m = vi & 63, rest = vi >> 6;
+        const int cc = rest % (D / 32), s = rest / (D / 32);
+        off[i] = (cc * 32 + (m & 31)) * (N / 2) + s * 32 + (m >> 5) * 16;
       }
     }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nV % NT == 0 || slot < nV) {
-        if constexpr (PV8) {
-          // One byte per key.  The FP8 operand's k order: lane half h holds keys
-          // 16 h + [0, 16) (bytes 0-15) and 32 + 16 h + [0, 16) (bytes 16-31) of
-          // the 64-key step, while its E8M0 byte still covers keys 32 h + [0, 32).
-          const int hh = slot & 1, m = (slot >> 1) & 63, rest = slot >> 7;
-          const int cc = rest % (D / 32), s = rest / (D / 32);
-          const int row = cc * 32 + (m & 31);
-          v[i] = *reinterpret_cast<const v4i*>(vc + (size_t)row * N + key0 + s * 64 + (m >> 5) * 16 + hh * 32);
-        } else {
-          const int m = slot & 63, rest = slot >> 6;
-          const int cc = rest % (D / 32), s = rest / (D / 32);
-          const int row = cc * 32 + (m & 31);
-          v[i] = *reinterpret_cast<const v4i*>(vc + (size_t)row * (N / 2) + key0 / 2 + s * 32 + (m >> 5) * 16);
-        }
-      }
-    }
-    if (tid < kBN) {
-      const uint8_t* p = ks_ + (size_t)(key0 + tid) * (D / 32);
-      ks = D == 128 ? *reinterpret_cast<const uint32_t*>(p) : (unsigned)*reinterpret_cast<const uint16_t*>(p);
-    } else if (tid < kBN + D) {
-      const int row = tid - kBN;
-      vs = *reinterpret_cast<const uint32_t*>(vs_ + (size_t)row * (N / 32) + key0 / 32);
-    }
+    const int r = wave * kPer + lane;
+    raw_off = r < L::rawK ? 4 * r : (r - L::rawK) * (N / 32);
   }
 
-  __device__ __forceinline__ void store(uint8_t* st, int tid) const {
+  __device__ __forceinline__ void issue(uint8_t* st, const uint8_t* kc, const uint8_t* ks, const uint8_t* vc,
+                                        const uint8_t* vs, int N, int key0) const {
+    const unsigned lds = lds_address(st);
+    const uint8_t* kb = kc + (size_t)key0 * (D / 2);
+    const uint8_t* vb = vc + (PV8 ? key0 : key0 / 2);
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nK % NT == 0 || slot < nK) *reinterpret_cast<v4i*>(st + L::kOff + slot * 16) = k[i];
+    for (int i = 0; i < kPerThread; ++i) {
+      const int item0 = wave * 64 + i * NT;  // wave-uniform
+      if (kItems % NT != 0 && item0 >= kItems) continue;
+      const bool is_k = item0 < nK;
+      lds_copy16(lds + (is_k ? L::kOff + item0 * 16 : L::vOff + (item0 - nK) * 16), is_k ? kb : vb, off[i]);
     }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int slot = tid + i * NT;
-      if (nV % NT == 0 || slot < nV) *reinterpret_cast<v4i*>(st + L::vOff + slot * 16) = v[i];
-    }
-    if (tid < kBN) {
-      const int sub = sub_of_key(tid), m0 = row_of_key(tid);
-      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::ksOff) + sub * 64;
-      dst[m0] = ks;            // lanes 0..31 use scale bytes 0, 2 (d blocks 0, 2)
-      dst[m0 + 32] = ks >> 8;  // lanes 32..63 use bytes 1, 3
-    } else if (tid < kBN + D) {
-      const int row = tid - kBN, cc = row >> 5, m0 = row & 31;
-      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::vsOff) + cc * 64;
-      dst[m0] = vs;
-      dst[m0 + 32] = vs >> 8;
+    const int r0 = wave * kPer;
+    const uint8_t* sb = r0 < L::rawK ? ks + (size_t)key0 * (D / 32) : vs + key0 / 32;
+    if (kPer == 64 || (threadIdx.x & 63) < kPer) lds_copy4(lds + L::rawOff + 4 * r0, sb, raw_off);
+  }
+
+  // The tile's E8M0 words in operand order: K word of key k at [sub][row] and,
+  // shifted by one byte, at [sub][row + 32] (lanes 0..31 take scale bytes 0 and 2
+  // of a word, lanes 32..63 bytes 1 and 3); V^T words likewise per 32-row chunk.
+  // Reads only the raw words this wave copied.
+  __device__ __forceinline__ static void arrange(uint8_t* st, int tid) {
+    const int lane = tid & 63, r = (tid >> 6) * kPer + lane;
+    if (lane >= kPer) return;
+    const unsigned raw = reinterpret_cast<const uint32_t*>(st + L::rawOff)[r];
+    auto put_k = [&](int key, unsigned w) {
+      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::ksOff) + sub_of_key(key) * 64 + row_of_key(key);
+      dst[0] = w;
+      dst[32] = w >> 8;
+    };
+    if (r < L::rawK) {
+      if constexpr (D == 128) {
+        put_k(r, raw);
+      } else {  // two keys of two bytes
+        put_k(2 * r, raw & 0xffff);
+        put_k(2 * r + 1, raw >> 16);
+      }
+    } else {
+      const int row = r - L::rawK;
+      uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::vsOff) + (row >> 5) * 64 + (row & 31);
+      dst[0] = raw;
+      dst[32] = raw >> 8;
     }
   }
 };
 
 // Two waves per SIMD, except where the LDS ring allows one workgroup of four
-// waves per CU only (FP8 V tiles with d = 128: 104 KiB).
+// waves per CU only (FP8 V tiles with d = 128: 108 KiB).
 template <int D, int NW, int VAR>
 constexpr int kMinWaves = ((VAR & kPV8) && NW == 4 && D == 128) ? 1 : 2;
 
@@ -218,7 +272,22 @@ fwd_mxfp4_kernel(const KParams p) {
   static_assert(EX2 == 0 || EX2 == 1 || EX2 == 2 || EX2 == 4 || EX2 == 8 || EX2 == 16, "pairs per 32-key block");
   using L = Layout<D, (VAR & kPV8) != 0>;
   constexpr int BM = NW * 32;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * L::stage];
+  // The LDS ring: one array per stage, so that the compiler tracks the
+  // direct-to-LDS copies per stage and waits for none of them before reading
+  // another stage.
+  __shared__ __attribute__((aligned(16))) uint8_t ring0[L::stage];
+  __shared__ __attribute__((aligned(16))) uint8_t ring1[L::stage];
+  __shared__ __attribute__((aligned(16))) uint8_t ring2[L::stage];
+  __shared__ __attribute__((aligned(16))) uint8_t ring3[L::stage];
+  static_assert(kStages == 4, "one array per ring stage");
+  auto ring = [&](auto B_) -> uint8_t* {
+    constexpr int b = decltype(B_)::value % kStages;
+    if constexpr (b == 0) return ring0;
+    else if constexpr (b == 1) return ring1;
+    else if constexpr (b == 2) return ring2;
+    else return ring3;
+  };
+  using I0 = std::integral_constant<int, 0>;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, lr = lane & 31;
@@ -401,7 +470,7 @@ fwd_mxfp4_kernel(const KParams p) {
           *reinterpret_cast<v8i*>(p.p_codes + (size_t)slot * N + (2 * g + h) * 32) = keyorder;
         }
       }
-      // Operand k order (see TileRegs::load): the lower half keeps keys 0-15 of
+      // Operand k order (see TileCopy::issue): the lower half keeps keys 0-15 of
       // block 0 and takes keys 0-15 of block 1; the upper half takes keys 16-31
       // of block 0 and keeps keys 16-31 of block 1.
 #pragma unroll
@@ -496,26 +565,26 @@ fwd_mxfp4_kernel(const KParams p) {
     }
   };
 
-  // Pipeline.  LDS holds a ring of kStages = 4 tiles; at the start of tile t the
-  // staged registers of tile t+1 are published and tile t+3 is fetched into the
-  // freed register set (two sets: even and odd tiles).  In 64-key step g the
-  // matrix unit runs PV of step g and QK of step g+2 while the vector ALU runs
-  // Direct-P of step g+1.  Steps are unrolled eight at a time (four tiles), so
-  // every LDS offset and register set is a compile-time constant.
-  // With four waves each thread stages twice the bytes, so only one set is kept
-  // and tiles are fetched two (not three) tiles ahead.
-  constexpr bool kTwoSets = NW == 8 && !PV8;  // FP8 V tiles double the staged bytes
-  constexpr int kAhead = kTwoSets ? 3 : 2;
-  TileRegs<D, NW, PV8> st_even;
-  TileRegs<D, kTwoSets ? NW : 0, PV8> st_odd;
-  st_even.load(kc, ks, vc, vs, N, 0, tid);
-  st_even.store(lds, tid);
-  if constexpr (kTwoSets) {
-    if (ntiles > 1) st_odd.load(kc, ks, vc, vs, N, kBN, tid);
-    if (ntiles > 2) st_even.load(kc, ks, vc, vs, N, 2 * kBN, tid);
-  } else {
-    if (ntiles > 1) st_even.load(kc, ks, vc, vs, N, kBN, tid);
-  }
+  // Pipeline.  LDS holds a ring of kStages = 4 tiles.  At the start of tile t
+  // each wave waits until its copies of tile t+1 have landed (only tile t+2's
+  // may still be in flight), puts the E8M0 words it copied into operand order,
+  // and after the barrier fetches tile t+3 into the stage of tile t-1, which
+  // every wave has finished reading.  Every publish fetches exactly one tile
+  // (past the end: the last tile again, into a stage nobody reads), so a wave's
+  // vmcnt always counts the same loads.  In 64-key step g the matrix unit runs
+  // PV of step g and QK of step g+2 while the vector ALU runs Direct-P of step
+  // g+1.  Steps are unrolled eight at a time (four tiles), so every LDS stage is
+  // a compile-time constant.
+  using Copy = TileCopy<D, NW, PV8>;
+  constexpr int kBatch = Copy::kLoads;
+  Copy copy;
+  copy.init(N, tid);
+  const int key1 = min(1, ntiles - 1) * kBN, key2 = min(2, ntiles - 1) * kBN;
+  copy.issue(ring(I0{}), kc, ks, vc, vs, N, 0);
+  copy.issue(ring(std::integral_constant<int, 1>{}), kc, ks, vc, vs, N, key1);
+  copy.issue(ring(std::integral_constant<int, 2>{}), kc, ks, vc, vs, N, key2);
+  vm_wait<2 * kBatch>();  // tile 0 has landed
+  Copy::arrange(ring(I0{}), tid);
   __syncthreads();
 
   // Two S^T buffers and two P operands alternate with the step parity.
@@ -525,8 +594,8 @@ fwd_mxfp4_kernel(const KParams p) {
   if constexpr (GUARD) {
     // Anchor (Alg. 3, steps 1-2): the largest score of the first key tile, which
     // holds the anchor keys; each lane half has two of its four 32-key blocks.
-    qk(lds, std::integral_constant<int, 0>{}, SB);
-    qk(lds, std::integral_constant<int, 1>{}, SA);
+    qk(ring(I0{}), std::integral_constant<int, 0>{}, SB);
+    qk(ring(I0{}), std::integral_constant<int, 1>{}, SA);
     float am = fmaxf(SB[0][0], SB[1][0]);
 #pragma unroll
     for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, SB[0][r]), SB[1][r]);
@@ -541,10 +610,10 @@ fwd_mxfp4_kernel(const KParams p) {
     }
     directp(SB, 0, PA, uA, std::false_type{});
   } else {
-    qk(lds, std::integral_constant<int, 0>{}, SA);
+    qk(ring(I0{}), std::integral_constant<int, 0>{}, SA);
     if constexpr (CAUSAL) causal_mask(SA, 0);
     directp(SA, 0, PA, uA, std::false_type{});
-    qk(lds, std::integral_constant<int, 1>{}, SA);
+    qk(ring(I0{}), std::integral_constant<int, 1>{}, SA);
   }
 
   // One step of the pipeline; j is the step's position in its group of eight.
@@ -553,8 +622,9 @@ fwd_mxfp4_kernel(const KParams p) {
     constexpr int j = decltype(J_)::value;
     constexpr bool guard = decltype(TAIL_)::value;
     constexpr int sl = j % 2;                 // step within its tile
-    constexpr int b_cur = (j / 2) % kStages;  // ring slot of tile t
-    constexpr int b_nxt = (j / 2 + 1) % kStages;
+    using b_cur = std::integral_constant<int, j / 2>;  // ring stage of tile t
+    using b_nxt = std::integral_constant<int, j / 2 + 1>;
+    using b_new = std::integral_constant<int, j / 2 + 3>;
     auto& S_in = (sl == 0) ? SA : SB;   // S^T of step g+1
     auto& S_out = (sl == 0) ? SB : SA;  // S^T of step g+2
     auto& P_cur = (sl == 0) ? PA : PB;  // P of step g
@@ -563,17 +633,14 @@ fwd_mxfp4_kernel(const KParams p) {
     auto& u_nxt = (sl == 0) ? uB : uA;
     const int t = g >> 1;
     if constexpr (sl == 0) {
-      auto publish = [&](auto& set) {  // `set` holds tile t+1
-        if (!guard || t + 1 < ntiles) set.store(lds + b_nxt * L::stage, tid);
-        __syncthreads();
-        if (t + kAhead < ntiles) set.load(kc, ks, vc, vs, N, (t + kAhead) * kBN, tid);
-      };
-      if constexpr (kTwoSets && (j / 2) % 2 == 0) publish(st_odd);
-      else publish(st_even);
+      vm_wait<kBatch>();  // tile t+1 has landed: only tile t+2's loads may be in flight
+      if (!guard || t + 1 < ntiles) Copy::arrange(ring(b_nxt{}), tid);
+      __syncthreads();
+      copy.issue(ring(b_new{}), kc, ks, vc, vs, N, min(t + 3, ntiles - 1) * kBN);
     }
-    pv(lds + b_cur * L::stage, std::integral_constant<int, sl>{}, P_cur, u_cur);
+    pv(ring(b_cur{}), std::integral_constant<int, sl>{}, P_cur, u_cur);
     if (!guard || g + 2 < nsteps) {
-      qk(lds + b_nxt * L::stage, std::integral_constant<int, sl>{}, S_out);
+      qk(ring(b_nxt{}), std::integral_constant<int, sl>{}, S_out);
       // Issue QK of step g+2 in this step (it would otherwise sink next to its
       // consumer in step g+1 and serialise with the code map); emits nothing.
       asm volatile("" ::"v"(S_out[0]), "v"(S_out[1]));
@@ -600,6 +667,7 @@ fwd_mxfp4_kernel(const KParams p) {
     const int g = g0 + decltype(J_)::value;
     if (g < nsteps) step(J_, std::true_type{}, g);
   });
+  vm_wait<0>();  // no copy may still be landing in LDS when the workgroup ends
 
   // Epilogue: O = acc / (6 D).  The denominator sits in register 0 of the lower half.
   float Dfin;  // query lane % 32
