@@ -119,31 +119,21 @@ __device__ __forceinline__ int key_of_row(int sub, int m) {
 __device__ __forceinline__ int sub_of_key(int k) { return 2 * (k >> 6) + ((k >> 4) & 1); }
 __device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4 * ((k >> 5) & 1) + (k & 3); }
 
-// Direct-to-LDS copies: lane l's 16 (4) bytes from `base` + `off` (a 64-bit
-// scalar base and this lane's 32-bit offset) land at LDS byte address `lds` +
-// 16 l (4 l), the LDS base being taken from M0.  Written as inline assembly so
-// that the compiler counts neither the loads nor the LDS they write (it would
-// otherwise wait for every copy in flight before each LDS read); the kernel
-// waits for its own copies with vm_wait before the barrier that publishes a
-// tile.  M0 is restored afterwards, and one wait state separates its write
-// from the load that reads it.
-__device__ __forceinline__ void lds_copy16(unsigned lds, const uint8_t* base, unsigned off) {
-  unsigned saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds), "v"(off), "s"(base)
-      : "memory");
+// Direct-to-LDS buffer copies: lane l's 16 (4) bytes at byte soff + off of the
+// buffer `rsrc` land at LDS byte address `lds` + 16 l (4 l); `lds` travels in
+// M0, and one wait state separates its write from the load.  Bytes past the
+// buffer's end read as zero, so a copy past the last tile is harmless.
+// Written as inline assembly so that the compiler counts neither the loads
+// nor the LDS they write (it would otherwise wait for every copy in flight
+// before each LDS read); the kernel waits for its own copies with vm_wait
+// before the barrier that publishes a tile.
+__device__ __forceinline__ void lds_copy16(unsigned lds, __amdgpu_buffer_rsrc_t rsrc, int soff, unsigned off) {
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(off), "s"(rsrc), "s"(soff), "{m0}"(lds)
+               : "memory");
 }
-__device__ __forceinline__ void lds_copy4(unsigned lds, const uint8_t* base, unsigned off) {
-  unsigned saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
-      "global_load_lds_dword %2, %3\n\ts_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds), "v"(off), "s"(base)
-      : "memory");
+__device__ __forceinline__ void lds_copy4(unsigned lds, __amdgpu_buffer_rsrc_t rsrc, int soff, unsigned off) {
+  asm volatile("s_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds" ::"v"(off), "s"(rsrc), "s"(soff), "{m0}"(lds)
+               : "memory");
 }
 // Wait until at most n of this wave's vector-memory operations are in flight.
 template <int n>
@@ -154,6 +144,10 @@ __device__ __forceinline__ void vm_wait() {
 __device__ __forceinline__ unsigned lds_address(const uint8_t* p) {
   return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
 }
+// Raw buffer over `bytes` bytes (gfx9 descriptor: 32-bit data format, no stride).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_buffer(const uint8_t* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, bytes, 0x00020000);
+}
 
 // One 128-key tile: K and V^T codes copied from global memory straight into an
 // LDS stage in operand order, and its E8M0 words copied raw, then rearranged
@@ -161,10 +155,12 @@ __device__ __forceinline__ unsigned lds_address(const uint8_t* p) {
 //   Codes: item i is one 16-byte operand fragment, K items first, then V^T
 //   items; thread tid copies items tid, tid + NT, ...  A wave's 64 lanes copy
 //   64 consecutive fragments, the order in which the direct-to-LDS load writes.
-//   Scales: kPer raw words per wave (lane l < kPer of wave w copies word
-//   w kPer + l), so every wave issues the same number of loads per tile.
-// The per-lane source offsets do not depend on the tile; only the scalar base
-// moves with the tile's first key.
+//   Scales: 64 raw words per block; wave w copies block w % kRawWaves, so
+//   with more waves than blocks two waves write the same bytes to the same
+//   place, and every wave issues the same number of loads per tile.
+// A copy reads one buffer of the (batch, head) at this lane's fixed offset
+// plus a per-tile scalar offset (key0 / 2) * mul (scales: (key0 / 32) * mul);
+// the buffer, the multiplier and the LDS position are fixed per wave.
 template <int D, int NW, bool PV8>
 struct TileCopy {
   using L = Layout<D, PV8>;
@@ -173,22 +169,32 @@ struct TileCopy {
   static constexpr int nV = L::vCodes / 16;
   static constexpr int kItems = nK + nV;
   static constexpr int kPerThread = (kItems + NT - 1) / NT;
-  static constexpr int kPer = (L::rawK + L::rawV) / NW;  // raw scale words per wave
-  static constexpr int kLoads = kItems / NT + 1;          // loads every wave issues per tile, at least
+  static constexpr int kRawWaves = (L::rawK + L::rawV) / 64;  // blocks of 64 raw words
+  static constexpr int kLoads = kItems / NT + 1;              // loads every wave issues per tile, at least
   static_assert(nK % 64 == 0 && nV % 64 == 0, "whole waves per operand");
-  static_assert(kPer * NW == L::rawK + L::rawV && kPer <= 64 && L::rawK % kPer == 0, "whole waves per scale operand");
+  static_assert(L::rawK % 64 == 0 && L::rawV % 64 == 0 && kRawWaves <= NW, "whole waves per scale operand");
 
-  unsigned off[kPerThread];  // this lane's byte offset from the tile's K or V^T base
-  unsigned raw_off;          // and from its K or V^T scale base
-  int wave;                  // wave-uniform
+  __amdgpu_buffer_rsrc_t buf[kPerThread], raw_buf;  // wave-uniform
+  int mul[kPerThread], raw_mul;                     // wave-uniform
+  unsigned lds_off[kPerThread], raw_lds;            // wave-uniform
+  unsigned off[kPerThread], raw_off;                // this lane's offsets
+  bool active[kPerThread];                          // wave-uniform
 
-  __device__ __forceinline__ void init(int N, int tid) {
-    wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  __device__ __forceinline__ void init(const uint8_t* kc, const uint8_t* ks, const uint8_t* vc, const uint8_t* vs,
+                                       int N, int tid) {
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
+    const __amdgpu_buffer_rsrc_t kbuf = make_buffer(kc, N * (D / 2));
+    const __amdgpu_buffer_rsrc_t vbuf = make_buffer(vc, D * (PV8 ? N : N / 2));
 #pragma unroll
     for (int i = 0; i < kPerThread; ++i) {
-      const int item = wave * 64 + i * NT + lane;
-      if (item < nK) {
+      const int item0 = wave * 64 + i * NT, item = item0 + lane;
+      active[i] = kItems % NT == 0 || item0 < kItems;
+      const bool is_k = (nK % NT == 0) ? (i < nK / NT) : item0 < nK;  // compile-time where it can be
+      buf[i] = is_k ? kbuf : vbuf;
+      mul[i] = is_k ? D : (PV8 ? 2 : 1);
+      lds_off[i] = is_k ? L::kOff + item0 * 16 : L::vOff + (item0 - nK) * 16;
+      if (is_k) {
         const int m = item & 63, rest = item >> 6;
         const int c = rest % (D / 64), sub = rest / (D / 64);
         off[i] = key_of_row(sub, m & 31) * (D / 2) + (2 * c + (m >> 5)) * 16;
@@ -207,34 +213,31 @@ struct TileCopy {
         off[i] = (cc * 32 + (m & 31)) * (N / 2) + s * 32 + (m >> 5) * 16;
       }
     }
-    const int r = wave * kPer + lane;
-    raw_off = r < L::rawK ? 4 * r : (r - L::rawK) * (N / 32);
+    const int rb = wave % kRawWaves, r = rb * 64 + lane;
+    const bool raw_k = rb * 64 < L::rawK;
+    raw_buf = raw_k ? make_buffer(ks, N * (D / 32)) : make_buffer(vs, D * (N / 32));
+    raw_mul = raw_k ? D : 1;  // per 32 keys: d / 32 bytes for each of 32 keys, or one byte
+    raw_lds = L::rawOff + rb * 256;
+    raw_off = raw_k ? 4 * r : (r - L::rawK) * (N / 32);
   }
 
-  __device__ __forceinline__ void issue(uint8_t* st, const uint8_t* kc, const uint8_t* ks, const uint8_t* vc,
-                                        const uint8_t* vs, int N, int key0) const {
+  // Fetch the tile of keys [key0, key0 + 128) into stage `st`.
+  __device__ __forceinline__ void issue(uint8_t* st, int key0) const {
     const unsigned lds = lds_address(st);
-    const uint8_t* kb = kc + (size_t)key0 * (D / 2);
-    const uint8_t* vb = vc + (PV8 ? key0 : key0 / 2);
+    const int half = key0 >> 1;
 #pragma unroll
-    for (int i = 0; i < kPerThread; ++i) {
-      const int item0 = wave * 64 + i * NT;  // wave-uniform
-      if (kItems % NT != 0 && item0 >= kItems) continue;
-      const bool is_k = item0 < nK;
-      lds_copy16(lds + (is_k ? L::kOff + item0 * 16 : L::vOff + (item0 - nK) * 16), is_k ? kb : vb, off[i]);
-    }
-    const int r0 = wave * kPer;
-    const uint8_t* sb = r0 < L::rawK ? ks + (size_t)key0 * (D / 32) : vs + key0 / 32;
-    if (kPer == 64 || (threadIdx.x & 63) < kPer) lds_copy4(lds + L::rawOff + 4 * r0, sb, raw_off);
+    for (int i = 0; i < kPerThread; ++i)
+      if (active[i]) lds_copy16(lds + lds_off[i], buf[i], half * mul[i], off[i]);
+    lds_copy4(lds + raw_lds, raw_buf, (key0 >> 5) * raw_mul, raw_off);
   }
 
   // The tile's E8M0 words in operand order: K word of key k at [sub][row] and,
   // shifted by one byte, at [sub][row + 32] (lanes 0..31 take scale bytes 0 and 2
   // of a word, lanes 32..63 bytes 1 and 3); V^T words likewise per 32-row chunk.
-  // Reads only the raw words this wave copied.
+  // Reads only raw words this wave copied itself.
   __device__ __forceinline__ static void arrange(uint8_t* st, int tid) {
-    const int lane = tid & 63, r = (tid >> 6) * kPer + lane;
-    if (lane >= kPer) return;
+    const int wave = tid >> 6, r = tid;  // wave w < kRawWaves arranges block w
+    if (wave >= kRawWaves) return;
     const unsigned raw = reinterpret_cast<const uint32_t*>(st + L::rawOff)[r];
     auto put_k = [&](int key, unsigned w) {
       uint32_t* dst = reinterpret_cast<uint32_t*>(st + L::ksOff) + sub_of_key(key) * 64 + row_of_key(key);
@@ -362,6 +365,14 @@ fwd_mxfp4_kernel(const KParams p) {
   // FP8: lane c < 32, register 0 = query c.
   std::conditional_t<PV8, v16f, v4f> Dacc = {};
   float Mref = -1.0e6f;  // integer row reference (exact in fp32); no block seen yet
+  // Carried with it: the rescale threshold M + tau and the E8M0 bias, so that a
+  // block's byte is one subtraction from E (all small integers, exact in fp32).
+  constexpr float kByteBias = PV8 ? 120.0f : 127.0f;
+  float Mthr = Mref + kTau, Mbias = Mref - kByteBias;
+  // -A / 8 held in a vector register: the code-map offset fma then reads one
+  // scalar operand only and needs no per-step copy (emits nothing).
+  float na8 = -p.a8;
+  asm volatile("" : "+v"(na8));
   float Rref = 0.0f;     // guard: fixed row reference from the anchor tile (Alg. 3)
 
   const int ntiles = CAUSAL ? (qt + 1) * BM / kBN : N / kBN;  // causal: keys up to the tile's last query
@@ -447,7 +458,7 @@ fwd_mxfp4_kernel(const KParams p) {
       // its codes at 0 instead of NaN (its E8M0 byte is 0 either way)
       T = CAUSAL ? fmaxf(E, -1.0e30f) : E;
     }
-    const float c0 = fmaf(-p.a8, T, p.k0_8);    // (A (log2 6 - T) + B) / 8
+    const float c0 = fmaf(na8, T, p.k0_8);      // (A (log2 6 - T) + B) / 8
     const float c1 = EX2 ? p.k1 - T : 0.0f;     // log2 6 - T, the exponent offset of 2^x
     if constexpr (PV8) {
       // FP8 payload: E4M3(2^(y - T + 7)) < 256 for every key (the block maximum
@@ -524,11 +535,11 @@ fwd_mxfp4_kernel(const KParams p) {
       // Online integer reference with a lazy, exact power-of-two rescale of what
       // PV has accumulated so far; the halves agree on the reference because the
       // branch is taken by the whole wave and uses both halves' exponents.
-      if (__builtin_amdgcn_ballot_w64(E > Mref + kTau)) {
+      if (__builtin_amdgcn_ballot_w64(E > Mthr)) {
         unsigned ea = as_uint(E), eb = ea;
         swap_halves(ea, eb);  // each lane: (block-0 exponent, block-1 exponent)
         const float Emax = fmaxf(as_float(ea), as_float(eb));
-        const float Mn = Emax > Mref + kTau ? Emax : Mref;
+        const float Mn = Emax > Mthr ? Emax : Mref;
         const int sh = (int)(Mref - Mn);
 #pragma unroll
         for (int c = 0; c < D / 32; ++c)
@@ -537,9 +548,11 @@ fwd_mxfp4_kernel(const KParams p) {
         Dacc[0] = ldexpf(Dacc[0], sh);
         if constexpr (!PV8) Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
         Mref = Mn;
+        Mthr = Mn + kTau;
+        Mbias = Mn - kByteBias;
       }
       // E8M0 byte of this lane's block: clamp(E - M + 127, 0, 254) (E - M <= kTau).
-      u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mref + (PV8 ? 120.0f : 127.0f), 0, 0u);
+      u = (int)__builtin_amdgcn_cvt_pk_u8_f32(E - Mbias, 0, 0u);
     }
     if constexpr (DUMP) {
       if (slot >= 0) {
@@ -570,19 +583,18 @@ fwd_mxfp4_kernel(const KParams p) {
   // may still be in flight), puts the E8M0 words it copied into operand order,
   // and after the barrier fetches tile t+3 into the stage of tile t-1, which
   // every wave has finished reading.  Every publish fetches exactly one tile
-  // (past the end: the last tile again, into a stage nobody reads), so a wave's
-  // vmcnt always counts the same loads.  In 64-key step g the matrix unit runs
+  // (past the end: zeros, into a stage nobody reads), so a wave's vmcnt always
+  // counts the same loads.  In 64-key step g the matrix unit runs
   // PV of step g and QK of step g+2 while the vector ALU runs Direct-P of step
   // g+1.  Steps are unrolled eight at a time (four tiles), so every LDS stage is
   // a compile-time constant.
   using Copy = TileCopy<D, NW, PV8>;
   constexpr int kBatch = Copy::kLoads;
   Copy copy;
-  copy.init(N, tid);
-  const int key1 = min(1, ntiles - 1) * kBN, key2 = min(2, ntiles - 1) * kBN;
-  copy.issue(ring(I0{}), kc, ks, vc, vs, N, 0);
-  copy.issue(ring(std::integral_constant<int, 1>{}), kc, ks, vc, vs, N, key1);
-  copy.issue(ring(std::integral_constant<int, 2>{}), kc, ks, vc, vs, N, key2);
+  copy.init(kc, ks, vc, vs, N, tid);
+  copy.issue(ring(I0{}), 0);
+  copy.issue(ring(std::integral_constant<int, 1>{}), kBN);
+  copy.issue(ring(std::integral_constant<int, 2>{}), 2 * kBN);
   vm_wait<2 * kBatch>();  // tile 0 has landed
   Copy::arrange(ring(I0{}), tid);
   __syncthreads();
@@ -632,23 +644,26 @@ fwd_mxfp4_kernel(const KParams p) {
     auto& P_nxt = (sl == 0) ? PB : PA;  // P of step g+1
     auto& u_nxt = (sl == 0) ? uB : uA;
     const int t = g >> 1;
+    // PV of step g and Direct-P of step g+1 read nothing the barrier publishes,
+    // so they come first: the matrix unit has PV's products in hand while the
+    // waves meet at the barrier.
+    pv(ring(b_cur{}), std::integral_constant<int, sl>{}, P_cur, u_cur);
+    if (!guard || g + 1 < nsteps) {
+      // masked steps all fall in the tail group (see the loop bound below)
+      if constexpr (CAUSAL && guard) causal_mask(S_in, g + 1);
+      directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
+    }
     if constexpr (sl == 0) {
       vm_wait<kBatch>();  // tile t+1 has landed: only tile t+2's loads may be in flight
       if (!guard || t + 1 < ntiles) Copy::arrange(ring(b_nxt{}), tid);
       __syncthreads();
-      copy.issue(ring(b_new{}), kc, ks, vc, vs, N, min(t + 3, ntiles - 1) * kBN);
+      copy.issue(ring(b_new{}), (t + 3) * kBN);
     }
-    pv(ring(b_cur{}), std::integral_constant<int, sl>{}, P_cur, u_cur);
     if (!guard || g + 2 < nsteps) {
       qk(ring(b_nxt{}), std::integral_constant<int, sl>{}, S_out);
       // Issue QK of step g+2 in this step (it would otherwise sink next to its
       // consumer in step g+1 and serialise with the code map); emits nothing.
       asm volatile("" ::"v"(S_out[0]), "v"(S_out[1]));
-    }
-    if (!guard || g + 1 < nsteps) {
-      // masked steps all fall in the tail group (see the loop bound below)
-      if constexpr (CAUSAL && guard) causal_mask(S_in, g + 1);
-      directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
     }
   };
 
