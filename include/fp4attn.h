@@ -40,7 +40,7 @@ extern "C" {
 typedef enum {
   FP4ATTN_OK = 0,
   FP4ATTN_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad size, enum or scalar */
-  FP4ATTN_ERR_UNSUPPORTED = 2, /* valid but not implemented (head dim not 64 or 128) */
+  FP4ATTN_ERR_UNSUPPORTED = 2, /* valid but not implemented (head dim not 64 or 128, N above 2^22, ...) */
   FP4ATTN_ERR_HIP = 3          /* the HIP runtime refused the launch; see fp4attn_last_error() */
 } fp4attn_status;
 
@@ -132,7 +132,7 @@ fp4attn_status fp4attn_quantize_mxfp4_anchored(const void* src, int src_dtype, i
  * Errors: INVALID_ARG for null/misaligned pointers, B < 1, H < 1, N < 128 or
  * N % 128 != 0, softmax_scale not finite or <= 0, affine_a not finite or <= 0,
  * affine_b not finite, bad out_dtype, or B*H*N beyond 2^31.  UNSUPPORTED for
- * d not in {64, 128}.  Non-finite operands (E8M0 byte 255) give unspecified but
+ * d not in {64, 128} or N above 4194304 (2^22) keys.  Non-finite operands (E8M0 byte 255) give unspecified but
  * non-faulting results for the rows they touch.
  */
 fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales,

@@ -38,6 +38,8 @@ bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr
     if (!aligned16(p)) return fail(FP4ATTN_ERR_INVALID_ARG, "%s is null or not 16-byte aligned", #p); \
   } while (0)
 
+constexpr int64_t kMaxN = int64_t(1) << 22;
+
 // Shared checks of the two attention forwards.
 fp4attn_status check_attention_shape(int64_t B, int64_t H, int64_t N, int64_t d, float softmax_scale, int out_dtype) {
   if (B < 1 || H < 1) return fail(FP4ATTN_ERR_INVALID_ARG, "B=%lld and H=%lld must be >= 1", (long long)B, (long long)H);
@@ -50,6 +52,8 @@ fp4attn_status check_attention_shape(int64_t B, int64_t H, int64_t N, int64_t d,
   if (B * H * N > (int64_t(1) << 31) - 1 || B * H > 65535 * 256)
     return fail(FP4ATTN_ERR_INVALID_ARG, "B*H*N=%lld exceeds 2^31", (long long)(B * H * N));
   if (d != 64 && d != 128) return fail(FP4ATTN_ERR_UNSUPPORTED, "head dimension d=%lld is not 64 or 128", (long long)d);
+  // one head's operands (FP8 V^T: d N bytes) and every in-head byte offset stay below 2^31
+  if (N > kMaxN) return fail(FP4ATTN_ERR_UNSUPPORTED, "N=%lld exceeds %lld keys", (long long)N, (long long)kMaxN);
   return FP4ATTN_OK;
 }
 

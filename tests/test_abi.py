@@ -63,6 +63,8 @@ def test_forward_validation(lib):
     assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 3, None) == 1
     assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, ctypes.c_void_p(4100), 0, None) == 1
     assert f(*FAKE[:6], 1 << 20, 1 << 10, 1 << 12, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1
+    # one head's operands must stay addressable with 32-bit offsets: N up to 2^22 keys
+    assert f(*FAKE[:6], 1, 1, (1 << 22) + 128, 128, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 2
 
 
 def test_quantize_and_bf16_validation(lib):
