@@ -6,11 +6,16 @@
 // r = 6|v| / 2^e_ceil, ceiling codes qc = E2M1(r) and floor codes qf = E2M1(2r),
 // the floor wins iff sum (2 qc - qf)(4 r - qf - 2 qc) < 0; every term of that
 // sum is exact in fp64 for fp32/bf16 inputs, so the choice is exact.
-// One thread owns one block; the kernel is HBM-bound.
+// bf16 inputs take a 32-bit path with the hardware E2M1 converter (exact too,
+// see mxfp4_block_bf16), 16-byte loads for Q and K and contiguous code rows
+// for V^T; fp32 inputs and odd shapes take the fp64 kernel.  One thread owns
+// one block (bf16 V^T: four blocks of two columns).
 #include "gfx950.hpp"
 #include "launch.hpp"
 
 namespace fp4attn {
+
+typedef float v2f __attribute__((ext_vector_type(2)));
 
 // Index k of the E2M1 magnitude {0, .5, 1, 1.5, 2, 3, 4, 6} nearest to r >= 0,
 // ties to even k, saturating: count the boundaries at or below r, each tie
@@ -123,6 +128,155 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_kernel(const T* __restrict
   scales[(b * outer + o) * nblk + blk] = (uint8_t)ubyte;
 }
 
+// bf16 fast path of the same rule, exact in 32-bit arithmetic.  A bf16 value
+// has at most 8 significant bits, so s = |v| / 2^e_ceil (<= 1) and r = 6 s are
+// exact in fp32, and the hardware converter's E2M1 rounding (nearest, ties to
+// the even code, saturating at 6) gives qc = E2M1(r) and qf = E2M1(min(2r, 6))
+// exactly; the decode instruction returns their values.  A term
+// A B = (2 qc - qf)(4 r - qf - 2 qc) is nonzero only for r > 1/8, where r is a
+// multiple of 2^-12, so each term is exact in fp32 and 4096 A B is an integer
+// below 2^21; the sum of 32 of them is exact in int32.  The codes of the chosen
+// amplitude are the ones already converted (unless the E8M0 range clamps it).
+//   raw[i]: elements 2i (bits 0-15) and 2i + 1 (bits 16-31).  Returns the E8M0
+//   byte; codes[j] holds elements 8 j .. 8 j + 7, even element in the low nibble.
+__device__ __forceinline__ unsigned mxfp4_block_bf16(const unsigned (&raw)[16], unsigned (&codes)[4]) {
+  float mag[32];
+  unsigned nonfinite = 0, sign[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const unsigned w = raw[i];
+    mag[2 * i] = __builtin_bit_cast(float, (w << 16) & 0x7fff0000u);
+    mag[2 * i + 1] = __builtin_bit_cast(float, w & 0x7fff0000u);
+    nonfinite |= ((w & 0x7f80u) == 0x7f80u) | ((w & 0x7f800000u) == 0x7f800000u);
+    // sign bits to code bit 3 of the even element's nibble and bit 7 of the odd one's
+    sign[i / 4] |= (((w >> 12) & 0x8u) | ((w >> 24) & 0x80u)) << (8 * (i % 4));
+  }
+  if (nonfinite) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) codes[j] = 0u;
+    return 255u;
+  }
+  float amax = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 32; ++j) amax = fmaxf(amax, mag[j]);
+  if (amax == 0.0f) {  // zero block: byte 0, code magnitudes 0, signs kept
+#pragma unroll
+    for (int j = 0; j < 4; ++j) codes[j] = sign[j];
+    return 0u;
+  }
+  int x;
+  const float m = frexpf(amax, &x);  // amax = m 2^x, m in [0.5, 1)
+  const int e_floor = x - 1, e_ceil = (m == 0.5f) ? x - 1 : x;
+  unsigned cc[4], cf[4];
+  int delta = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    unsigned wc = 0u, wf = 0u;
+    static_for<4>([&](auto P_) {
+      constexpr int pb = decltype(P_)::value;
+      const int k = 8 * j + 2 * pb;
+      const float r0 = 6.0f * ldexpf(mag[k], -e_ceil), r1 = 6.0f * ldexpf(mag[k + 1], -e_ceil);
+      wc = cvt_pk_fp4<pb>(pb == 0 ? 0u : wc, r0, r1, 1.0f);
+      wf = cvt_pk_fp4<pb>(pb == 0 ? 0u : wf, fminf(2.0f * r0, 6.0f), fminf(2.0f * r1, 6.0f), 1.0f);
+      const v2f qc = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wc, 1.0f, pb);
+      const v2f qf = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wf, 1.0f, pb);
+      const float t0 = fmaf(2.0f, qc[0], -qf[0]) * fmaf(4.0f, r0, -fmaf(2.0f, qc[0], qf[0]));
+      const float t1 = fmaf(2.0f, qc[1], -qf[1]) * fmaf(4.0f, r1, -fmaf(2.0f, qc[1], qf[1]));
+      delta += (int)(t0 * 4096.0f) + (int)(t1 * 4096.0f);
+    });
+    cc[j] = wc;
+    cf[j] = wf;
+  }
+  int e = (e_floor != e_ceil && delta < 0) ? e_floor : e_ceil;
+  e = e < -127 ? -127 : (e > 127 ? 127 : e);
+  if (e == e_ceil) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) codes[j] = cc[j] | sign[j];
+  } else if (e == e_floor) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) codes[j] = cf[j] | sign[j];
+  } else {  // amplitude clamped to the E8M0 range
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      unsigned w = 0u;
+      static_for<4>([&](auto P_) {
+        constexpr int pb = decltype(P_)::value;
+        const int k = 8 * j + 2 * pb;
+        w = cvt_pk_fp4<pb>(pb == 0 ? 0u : w, 6.0f * ldexpf(mag[k], -e), 6.0f * ldexpf(mag[k + 1], -e), 1.0f);
+      });
+      codes[j] = w | sign[j];
+    }
+  }
+  return (unsigned)(e + 127);
+}
+
+// bf16, blocks along the contiguous axis (Q, K): one block per thread, four
+// 16-byte loads.
+__global__ __launch_bounds__(256) void quantize_mxfp4_bf16_rows_kernel(const uint16_t* __restrict__ src, int64_t batch,
+                                                                       int64_t rows, int64_t cols,
+                                                                       uint8_t* __restrict__ codes,
+                                                                       uint8_t* __restrict__ scales, int64_t n_anchor,
+                                                                       int64_t anchor_stride) {
+  const int64_t nblk = cols / 32;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= batch * rows * nblk) return;
+  const int64_t blk = t % nblk, o = (t / nblk) % rows, b = t / (nblk * rows);
+  const uint4* p = reinterpret_cast<const uint4*>(src + (b * rows + anchor_source_row(o, n_anchor, anchor_stride)) * cols +
+                                                  blk * 32);
+  unsigned raw[16];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint4 q = p[i];
+    raw[4 * i] = q.x;
+    raw[4 * i + 1] = q.y;
+    raw[4 * i + 2] = q.z;
+    raw[4 * i + 3] = q.w;
+  }
+  unsigned w[4];
+  const unsigned u = mxfp4_block_bf16(raw, w);
+  *reinterpret_cast<v4i*>(codes + t * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  scales[t] = (uint8_t)u;
+}
+
+// bf16, blocks along rows with transposed output (V): a thread takes two
+// adjacent columns (one 4-byte load per row) and four consecutive blocks of
+// each, so its codes for a column are 64 contiguous bytes.  cols % 2 == 0 and
+// (rows / 32) % 4 == 0.
+__global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_kernel(const uint16_t* __restrict__ src, int64_t batch,
+                                                                       int64_t rows, int64_t cols,
+                                                                       uint8_t* __restrict__ codes,
+                                                                       uint8_t* __restrict__ scales, int64_t n_anchor,
+                                                                       int64_t anchor_stride) {
+  const int64_t nblk = rows / 32, npair = cols / 2, ngrp = nblk / 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= batch * ngrp * npair) return;
+  const int64_t cp = t % npair, grp = (t / npair) % ngrp, b = t / (npair * ngrp);
+  const uint16_t* base = src + b * rows * cols + 2 * cp;
+  const int64_t col0 = b * cols + 2 * cp;
+  unsigned u0 = 0u, u1 = 0u;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int64_t blk = grp * 4 + g;
+    unsigned pair[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+      pair[j] = *reinterpret_cast<const unsigned*>(base + anchor_source_row(blk * 32 + j, n_anchor, anchor_stride) * cols);
+    unsigned raw0[16], raw1[16];  // column 2 cp and 2 cp + 1, rows in order
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      raw0[i] = (pair[2 * i] & 0xffffu) | (pair[2 * i + 1] << 16);
+      raw1[i] = (pair[2 * i] >> 16) | (pair[2 * i + 1] & 0xffff0000u);
+    }
+    unsigned w[4];
+    u0 |= mxfp4_block_bf16(raw0, w) << (8 * g);
+    *reinterpret_cast<v4i*>(codes + (col0 * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+    u1 |= mxfp4_block_bf16(raw1, w) << (8 * g);
+    *reinterpret_cast<v4i*>(codes + ((col0 + 1) * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  }
+  *reinterpret_cast<unsigned*>(scales + col0 * nblk + grp * 4) = u0;
+  *reinterpret_cast<unsigned*>(scales + (col0 + 1) * nblk + grp * 4) = u1;
+}
+
 // MXFP8 (E4M3 payload + E8M0 per 32 values): the amplitude is the smallest
 // power of two 2^e with amax / 2^e <= 448, so no payload saturates; payloads
 // are v / 2^e (exact) rounded to nearest even by the hardware converter, which
@@ -222,6 +376,17 @@ hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, 
   const int64_t outer = axis == 1 ? rows : cols;
   const int64_t total = batch * outer * nblk;
   const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  if (src_dtype == 1 && axis == 1) {
+    hipLaunchKernelGGL(quantize_mxfp4_bf16_rows_kernel, grid, block, 0, stream, (const uint16_t*)src, batch, rows, cols,
+                       codes, scales, n_anchor, stride);
+    return hipGetLastError();
+  }
+  if (src_dtype == 1 && axis == 0 && cols % 2 == 0 && nblk % 4 == 0) {
+    const int64_t threads = batch * (nblk / 4) * (cols / 2);
+    hipLaunchKernelGGL(quantize_mxfp4_bf16_cols_kernel, dim3((unsigned)((threads + 255) / 256)), block, 0, stream,
+                       (const uint16_t*)src, batch, rows, cols, codes, scales, n_anchor, stride);
+    return hipGetLastError();
+  }
   if (src_dtype == 0) {
     if (axis == 1)
       hipLaunchKernelGGL((quantize_mxfp4_kernel<float, 1>), grid, block, 0, stream, (const float*)src, batch, rows,

@@ -62,6 +62,50 @@ def test_adversarial_blocks(fa, axis):
     _check(fa, x.to(torch.float32).reshape(1, *x.shape), axis)
 
 
+def _adversarial_bf16_blocks():
+    """32 blocks of 32 bf16 values: table values, rounding ties, zero and signed
+    zero, subnormals, amplitudes clamped at either end of the E8M0 range,
+    non-finite values and random blocks over 40 binades."""
+    mags = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+    mids = torch.tensor([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0])
+    blocks = [torch.cat([mags, -mags, mags / 6 * 4, -mags / 3]),
+              torch.cat([mids, mids / 2, -mids / 4, mids * 2 / 3]),
+              torch.cat([mids * 3 / 8, -mids * 5 / 16, mids / 12, mids * 7 / 24]),
+              torch.zeros(32)]
+    z = torch.zeros(32)
+    z[3] = -0.0
+    z[17] = -0.0
+    blocks.append(z)
+    blocks.append(torch.linspace(-1, 1, 32) * 2.0 ** -128)                 # subnormal bf16
+    blocks.append(torch.full((32,), 2.0 ** -131) * torch.arange(32))          # amplitude below 2^-127
+    blocks.append(torch.linspace(-1, 1, 32) * 3.0e38)                        # amplitude above 2^127
+    w = torch.ones(32)
+    w[0] = 2.0 ** 30
+    blocks.append(w * torch.linspace(-1, 1, 32))
+    nan = torch.randn(32, generator=torch.Generator().manual_seed(1))
+    nan[5] = float("nan")
+    blocks.append(nan)
+    inf = torch.randn(32, generator=torch.Generator().manual_seed(2))
+    inf[9] = -float("inf")
+    blocks.append(inf)
+    g = torch.Generator().manual_seed(3)
+    while len(blocks) < 32:
+        blocks.append(torch.randn(32, generator=g) * float(2.0 ** torch.randint(-20, 20, (1,), generator=g)))
+    return torch.stack(blocks).to(torch.bfloat16)                            # [32 blocks, 32]
+
+
+@pytest.mark.parametrize("axis", [-1, -2])
+def test_adversarial_blocks_bf16(fa, axis):
+    """The bf16 kernels: one block per row (axis -1), or four blocks of 32 rows
+    down each of 8 columns (axis -2), so both layouts of the fast path run."""
+    x = _adversarial_bf16_blocks()
+    if axis == -1:
+        x = x.reshape(1, 32, 32)
+    else:                                      # block (g, c) = rows 32 g .. 32 g + 31 of column c
+        x = x.reshape(4, 8, 32).permute(0, 2, 1).reshape(1, 128, 8).contiguous()
+    _check(fa, x, axis)
+
+
 @pytest.mark.parametrize("name", list(workloads.WORKLOADS))
 def test_workload_operands(fa, name):
     """Bit-exact on the workloads: every block for small ones; for large ones the
