@@ -7,15 +7,16 @@
 // the floor wins iff sum (2 qc - qf)(4 r - qf - 2 qc) < 0; every term of that
 // sum is exact in fp64 for fp32/bf16 inputs, so the choice is exact.
 // bf16 inputs take a 32-bit path with the hardware E2M1 converter (exact too,
-// see mxfp4_block_bf16), 16-byte loads for Q and K and contiguous code rows
+// see mxfp4_block_bf16), 16-byte loads for Q and K and two columns per thread
 // for V^T; fp32 inputs and odd shapes take the fp64 kernel.  One thread owns
-// one block (bf16 V^T: four blocks of two columns).
+// one block (bf16 V^T: one block of each of two columns).
 #include "gfx950.hpp"
 #include "launch.hpp"
 
 namespace fp4attn {
 
 typedef float v2f __attribute__((ext_vector_type(2)));
+
 
 // Index k of the E2M1 magnitude {0, .5, 1, 1.5, 2, 3, 4, 6} nearest to r >= 0,
 // ties to even k, saturating: count the boundaries at or below r, each tie
@@ -238,43 +239,36 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_bf16_rows_kernel(const uin
   scales[t] = (uint8_t)u;
 }
 
-// bf16, blocks along rows with transposed output (V): a thread takes two
-// adjacent columns (one 4-byte load per row) and four consecutive blocks of
-// each, so its codes for a column are 64 contiguous bytes.  cols % 2 == 0 and
-// (rows / 32) % 4 == 0.
+// bf16, blocks along rows with transposed output (V): a thread takes one block
+// of two adjacent columns (one 4-byte load per row; a wave reads 256-byte row
+// segments).  cols % 2 == 0.  (Several blocks per thread, for longer runs of
+// contiguous code bytes, measured slower: fewer waves in flight.)
 __global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_kernel(const uint16_t* __restrict__ src, int64_t batch,
                                                                        int64_t rows, int64_t cols,
                                                                        uint8_t* __restrict__ codes,
                                                                        uint8_t* __restrict__ scales, int64_t n_anchor,
                                                                        int64_t anchor_stride) {
-  const int64_t nblk = rows / 32, npair = cols / 2, ngrp = nblk / 4;
+  const int64_t nblk = rows / 32, npair = cols / 2;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= batch * ngrp * npair) return;
-  const int64_t cp = t % npair, grp = (t / npair) % ngrp, b = t / (npair * ngrp);
+  if (t >= batch * nblk * npair) return;
+  const int64_t cp = t % npair, blk = (t / npair) % nblk, b = t / (npair * nblk);
   const uint16_t* base = src + b * rows * cols + 2 * cp;
-  const int64_t col0 = b * cols + 2 * cp;
-  unsigned u0 = 0u, u1 = 0u;
+  unsigned pair[32];
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const int64_t blk = grp * 4 + g;
-    unsigned pair[32];
+  for (int j = 0; j < 32; ++j)
+    pair[j] = *reinterpret_cast<const unsigned*>(base + anchor_source_row(blk * 32 + j, n_anchor, anchor_stride) * cols);
+  unsigned raw0[16], raw1[16];  // column 2 cp and 2 cp + 1, rows in order
 #pragma unroll
-    for (int j = 0; j < 32; ++j)
-      pair[j] = *reinterpret_cast<const unsigned*>(base + anchor_source_row(blk * 32 + j, n_anchor, anchor_stride) * cols);
-    unsigned raw0[16], raw1[16];  // column 2 cp and 2 cp + 1, rows in order
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      raw0[i] = (pair[2 * i] & 0xffffu) | (pair[2 * i + 1] << 16);
-      raw1[i] = (pair[2 * i] >> 16) | (pair[2 * i + 1] & 0xffff0000u);
-    }
-    unsigned w[4];
-    u0 |= mxfp4_block_bf16(raw0, w) << (8 * g);
-    *reinterpret_cast<v4i*>(codes + (col0 * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-    u1 |= mxfp4_block_bf16(raw1, w) << (8 * g);
-    *reinterpret_cast<v4i*>(codes + ((col0 + 1) * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  for (int i = 0; i < 16; ++i) {
+    raw0[i] = (pair[2 * i] & 0xffffu) | (pair[2 * i + 1] << 16);
+    raw1[i] = (pair[2 * i] >> 16) | (pair[2 * i + 1] & 0xffff0000u);
   }
-  *reinterpret_cast<unsigned*>(scales + col0 * nblk + grp * 4) = u0;
-  *reinterpret_cast<unsigned*>(scales + (col0 + 1) * nblk + grp * 4) = u1;
+  const int64_t col0 = b * cols + 2 * cp;
+  unsigned w[4];
+  scales[col0 * nblk + blk] = (uint8_t)mxfp4_block_bf16(raw0, w);
+  *reinterpret_cast<v4i*>(codes + (col0 * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  scales[(col0 + 1) * nblk + blk] = (uint8_t)mxfp4_block_bf16(raw1, w);
+  *reinterpret_cast<v4i*>(codes + ((col0 + 1) * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
 }
 
 // MXFP8 (E4M3 payload + E8M0 per 32 values): the amplitude is the smallest
@@ -381,8 +375,8 @@ hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, 
                        codes, scales, n_anchor, stride);
     return hipGetLastError();
   }
-  if (src_dtype == 1 && axis == 0 && cols % 2 == 0 && nblk % 4 == 0) {
-    const int64_t threads = batch * (nblk / 4) * (cols / 2);
+  if (src_dtype == 1 && axis == 0 && cols % 2 == 0) {
+    const int64_t threads = batch * nblk * (cols / 2);
     hipLaunchKernelGGL(quantize_mxfp4_bf16_cols_kernel, dim3((unsigned)((threads + 255) / 256)), block, 0, stream,
                        (const uint16_t*)src, batch, rows, cols, codes, scales, n_anchor, stride);
     return hipGetLastError();
