@@ -127,12 +127,16 @@ __device__ __forceinline__ int row_of_key(int k) { return 8 * ((k >> 2) & 3) + 4
 // nor the LDS they write (it would otherwise wait for every copy in flight
 // before each LDS read); the kernel waits for its own copies with vm_wait
 // before the barrier that publishes a tile.
+// (`lds` and `soff` are wave-uniform; reading them from the first lane keeps
+// them in scalar registers whatever the compiler's uniformity analysis says.)
 __device__ __forceinline__ void lds_copy16(unsigned lds, __amdgpu_buffer_rsrc_t rsrc, int soff, unsigned off) {
-  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(off), "s"(rsrc), "s"(soff), "{m0}"(lds)
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(off), "s"(rsrc),
+               "s"(__builtin_amdgcn_readfirstlane(soff)), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
                : "memory");
 }
 __device__ __forceinline__ void lds_copy4(unsigned lds, __amdgpu_buffer_rsrc_t rsrc, int soff, unsigned off) {
-  asm volatile("s_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds" ::"v"(off), "s"(rsrc), "s"(soff), "{m0}"(lds)
+  asm volatile("s_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds" ::"v"(off), "s"(rsrc),
+               "s"(__builtin_amdgcn_readfirstlane(soff)), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
                : "memory");
 }
 // Wait until at most n of this wave's vector-memory operations are in flight.
@@ -145,8 +149,13 @@ __device__ __forceinline__ unsigned lds_address(const uint8_t* p) {
   return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
 }
 // Raw buffer over `bytes` bytes (gfx9 descriptor: 32-bit data format, no stride).
+// Base and size are the same in every lane; reading them from the first lane
+// keeps the descriptor in scalar registers, as the copy instructions require.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_buffer(const uint8_t* base, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, bytes, 0x00020000);
+  const uint64_t a = (uint64_t)base;
+  const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)a), hi = __builtin_amdgcn_readfirstlane((unsigned)(a >> 32));
+  uint8_t* b = (uint8_t*)(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(b, (short)0, __builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 
 // One 128-key tile: K and V^T codes copied from global memory straight into an
