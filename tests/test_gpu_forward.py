@@ -1,7 +1,7 @@
 """GPU parity of the Direct-P MXFP4 forward against the oracle.
 
-Gates (the benchmark spec): Direct-P code mismatch fraction <= 1e-4, output
-relative L2 <= 2e-3 and cosine >= 0.9999; all rows for the small workloads,
+Gates: Direct-P code mismatch fraction <= 1e-4, output relative L2 <= 2e-3
+and cosine >= 0.9999; all rows for the small workloads,
 4096 sampled rows (the same launch as the timed forward) for the large ones.
 """
 import numpy as np
@@ -78,6 +78,16 @@ def test_wide_launch_sampled(fa):
     q, k, v = (torch.randn(B, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
     host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
     _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, B * H * N, 7), "wide")
+
+
+def test_wide_launch_two_tiles(fa):
+    """The 8-wave path with two key tiles per head: the tile fetches run three tiles
+    ahead, so most of them read past the head's last key (zeros, never used)."""
+    g = torch.Generator().manual_seed(8)
+    B, H, N, d = 1, 256, 256, 128
+    q, k, v = (torch.randn(B, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, B * H * N, 5), "wide two tiles")
 
 
 @pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "student_t_b1h32_n8192_d128",
