@@ -592,8 +592,8 @@ fwd_mxfp4_kernel(const KParams p) {
   // may still be in flight), puts the E8M0 words it copied into operand order,
   // and after the barrier fetches tile t+3 into the stage of tile t-1, which
   // every wave has finished reading.  Every publish fetches exactly one tile
-  // (past the end: zeros, into a stage nobody reads), so a wave's vmcnt always
-  // counts the same loads.  In 64-key step g the matrix unit runs
+  // (past the end: bounds-checked bytes, zero past each buffer's end, into a
+  // stage nobody reads), so a wave's vmcnt always counts the same loads.  In 64-key step g the matrix unit runs
   // PV of step g and QK of step g+2 while the vector ALU runs Direct-P of step
   // g+1.  Steps are unrolled eight at a time (four tiles), so every LDS stage is
   // a compile-time constant.
