@@ -162,8 +162,10 @@ def measured_clock_ghz(torch, fa, ops, w, launches=5):
     return cyc / (ticks / 100e6) / 1e9
 
 
-def cpu_oracle_baseline(w, budget_s=12.0):
-    """Time the oracle (as it stands) on consecutive rows of head (0, 0) until the budget is spent."""
+def cpu_oracle_baseline(w, q, k, v, budget_s=12.0):
+    """Time the oracle (as it stands) on consecutive rows of head (0, 0) of the bench
+    inputs (CPU tensors q, k, v [B, H, N, d]) until the budget is spent.  Returns the
+    record and the oracle's output rows, for the parity check."""
     import numpy as np
     import workloads
     from oracle import directp, mxfp4
@@ -172,16 +174,17 @@ def cpu_oracle_baseline(w, budget_s=12.0):
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # threadpoolctl missing: report the affinity set
         threads = len(os.sched_getaffinity(0))
-    q, k, v = workloads.generate(w, B=1, H=1)
-    q64, k64, v64 = (workloads.as_f64(t)[0, 0] for t in (q, k, v))
+    q64, k64, v64 = (workloads.as_f64(t[:1, :1])[0, 0] for t in (q, k, v))
     t0 = time.perf_counter()
     kc, ks = mxfp4.quantize(k64, axis=-1)
     vc, vs = mxfp4.quantize(v64, axis=-2)
     rows_done = 0
     chunk = 128
+    outs = []
     while rows_done < w.N and time.perf_counter() - t0 < budget_s:
         qc, qs = mxfp4.quantize(q64[rows_done:rows_done + chunk], axis=-1)
-        directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(chunk), w.softmax_scale, want_codes=False)
+        outs.append(directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(chunk), w.softmax_scale,
+                                         want_codes=False)["O"])
         rows_done += chunk
     dt = time.perf_counter() - t0
     flops = 4.0 * rows_done * w.N * w.d
@@ -194,7 +197,7 @@ def cpu_oracle_baseline(w, budget_s=12.0):
                   f"including the oracle's own MXFP4 quantization of that head's K and V; {dt:.1f} s",
         "seconds": round(dt, 2),
         "full_workload_estimate_s": round(dt * w.rows / rows_done, 1),
-    }
+    }, np.concatenate(outs)
 
 
 def main():
@@ -229,7 +232,8 @@ def main():
     w = workloads.WORKLOADS[name]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    q, k, v = (t.to(dev) for t in workloads.generate(w))
+    q_cpu, k_cpu, v_cpu = workloads.generate(w)
+    q, k, v = (t.to(dev) for t in (q_cpu, k_cpu, v_cpu))
     torch.cuda.synchronize()
 
     ops = fa.quantize_qkv(q, k, v)
@@ -355,9 +359,21 @@ def main():
         "wall_ms_timed_region": round(wall_ms, 3),
         "roofline": roof,
         "gpu": torch.cuda.get_device_name(dev),
+        "gfx_target": torch.cuda.get_device_properties(dev).gcnArchName,
+        "kernel_source_sha256": _source_sha(),
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_oracle_baseline(w)
+        import numpy as np
+        line["cpu_baseline"], o_ref = cpu_oracle_baseline(w, q_cpu, k_cpu, v_cpu)
+        # parity of the timed launch on the rows the oracle computed (head (0, 0))
+        fp4_step()
+        torch.cuda.synchronize()
+        got = out[0, 0, :len(o_ref)].double().cpu().numpy()
+        rel = float(np.linalg.norm(got - o_ref) / np.linalg.norm(o_ref))
+        cos = float(np.sum(got * o_ref) / (np.linalg.norm(got) * np.linalg.norm(o_ref)))
+        line["parity"] = {"rows": int(len(o_ref)), "head": [0, 0], "o_rel_l2": rel, "o_cos": cos,
+                          "gate": {"o_rel_l2_max": 2e-3, "o_cos_min": 0.9999},
+                          "pass": bool(rel <= 2e-3 and cos >= 0.9999)}
     print(json.dumps(line), flush=True)
 
 
