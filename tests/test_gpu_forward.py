@@ -97,6 +97,65 @@ def test_full_size_sampled_rows(fa, name):
     _run_and_check(fa, host64, dev, workloads.sampled_rows(name), name)
 
 
+def _check_byte_operands(fa, ops_cpu, rows, label):
+    """Forward and Direct-P dump of MXFP4 operand bytes against the oracle on the
+    flattened query ``rows`` (the same bytes feed both sides)."""
+    from oracle import directp
+    B, H, N, half_d = ops_cpu[0].shape
+    d = 2 * half_d
+    s = 1.0 / np.sqrt(d)
+    rows = np.asarray(rows, dtype=np.int64)
+    print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)}: GPU launches", flush=True)
+    ops = tuple(t.cuda() for t in ops_cpu)
+    row_ids = torch.from_numpy(rows).cuda()
+    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s)
+    out = fa.forward_mxfp4(*ops, softmax_scale=s)
+    torch.cuda.synchronize()
+    assert torch.equal(out, dump["out"]), f"{label}: debug launch output differs from the forward"
+    assert bool(torch.isfinite(out).all()), f"{label}: non-finite output"
+    got = out.reshape(-1, d)[row_ids].cpu().numpy()
+    del ops, out
+    dump = {key: val for key, val in dump.items() if key != "out"}
+    print(f"[{label}] oracle", flush=True)
+    ref = {"O": [], "E": [], "M": [], "D": [], "codes": []}
+    order = []
+    for bh in np.unique(rows // N):
+        b, h = divmod(int(bh), H)
+        sel = np.nonzero(rows // N == bh)[0]
+        res = directp.forward_rows(*(t[b, h].numpy() for t in ops_cpu), rows[sel] % N, s)
+        for key in ref:
+            ref[key].append(res[key])
+        order.append(sel)
+    order = np.concatenate(order)
+    ref = {key: np.concatenate(val)[np.argsort(order)] for key, val in ref.items()}
+    mismatch = check_directp_dump(dump, ref, label)
+    rel, cos = rel_l2_cos(got, ref["O"])
+    print(f"[{label}] code mismatch {mismatch:.2e}  O rel-L2 {rel:.3e}  cos {cos:.8f}", flush=True)
+    assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{label}: rel {rel} cos {cos}"
+
+
+def test_longest_sequence_sampled_rows(fa):
+    """N = 2^22 keys, the largest the entry point accepts: every byte offset within
+    the head near its 32-bit limit, 32768 key tiles per workgroup.  Rows: the first
+    and last of the sequence, of a query tile and of a workgroup, and random ones."""
+    N = 1 << 22
+    ops_cpu = workloads.random_mxfp4_operands(1, 1, N, 128, seed=22)
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, N // 2 + 31, N - 257, N - 256, N - 1],
+                                     np.random.default_rng(22).integers(0, N, 8)]))
+    _check_byte_operands(fa, ops_cpu, rows, "N=2^22")
+
+
+def test_largest_grid_sampled_rows(fa):
+    """More than 2^16 (batch, head) slices in one launch; rows of the first, the
+    last and random slices."""
+    B, H, N = 2, 32775, 256
+    ops_cpu = workloads.random_mxfp4_operands(B, H, N, 64, seed=16)
+    rng = np.random.default_rng(16)
+    heads = np.unique(np.concatenate([[0, 1, H - 1, H, B * H - 2, B * H - 1], rng.integers(0, B * H, 10)]))
+    rows = np.unique(np.concatenate([bh * N + np.array([0, 1, 127, 128, N - 1]) for bh in heads]))
+    _check_byte_operands(fa, ops_cpu, rows, f"B{B} H{H}")
+
+
 def test_affine_variant_and_scale(fa):
     """The Wan fit (A, B) = (1.6, 0.95) and a non-default softmax scale."""
     host64, dev = load_workload("small_b1h8_n1024_d64", H=2)

@@ -45,3 +45,29 @@ def test_sampled_rows():
     assert len(r) == 4096 and np.all(np.diff(r) > 0) and r.max() < 32 * 16384
     assert np.array_equal(r, workloads.sampled_rows("long_b1h32_n16384_d128"))
     assert len(workloads.sampled_rows("tiny_b1h1_n128_d64")) == 128
+
+
+def test_random_mxfp4_operands_shapes_and_ranges():
+    ops = workloads.random_mxfp4_operands(2, 3, 256, 128, seed=5)
+    shapes = [(2, 3, 256, 64), (2, 3, 256, 4), (2, 3, 256, 64), (2, 3, 256, 4), (2, 3, 128, 128), (2, 3, 128, 8)]
+    assert [tuple(t.shape) for t in ops] == shapes
+    assert all(t.dtype == torch.uint8 for t in ops)
+    for t in ops[1::2]:
+        assert int(t.min()) >= 125 and int(t.max()) <= 129
+    assert int(ops[0].min()) == 0 and int(ops[0].max()) == 255
+    again = workloads.random_mxfp4_operands(2, 3, 256, 128, seed=5)
+    assert all(torch.equal(a, b) for a, b in zip(ops, again))
+
+
+def test_random_mxfp4_operand_scores_are_exact_in_fp32():
+    """The oracle refuses scores that fp32 cannot hold exactly; the band's extreme
+    bytes (largest magnitude codes at the largest and smallest scales) stay exact."""
+    from oracle import directp, mxfp4
+    ops = [t[0, 0].numpy() for t in workloads.random_mxfp4_operands(1, 1, 256, 128, seed=6)]
+    directp.raw_scores(mxfp4.scaled_operand(ops[0], ops[1]), mxfp4.scaled_operand(ops[2], ops[3]))
+    big = np.full((2, 64), 0x77, dtype=np.uint8)
+    for sq, sk in ((129, 129), (125, 129), (125, 125)):
+        q6 = mxfp4.scaled_operand(big, np.full((2, 4), sq, dtype=np.uint8))
+        k6 = mxfp4.scaled_operand(big, np.full((2, 4), sk, dtype=np.uint8))
+        raw = directp.raw_scores(q6, k6)
+        assert np.all(raw == 128 * 36.0 * 2.0 ** (sq + sk - 254))

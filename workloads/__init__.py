@@ -26,6 +26,13 @@ Tensors are then cast to the workload dtype (round to nearest even for bf16).
 Sampled query rows for large workloads are
 ``randperm(B*H*N, generator=manual_seed(seed + 1000))[:4096]`` over flattened
 ``(b*H + h)*N + i`` indices.
+
+Size-limit cases (the longest sequence, the largest grid) take their operands
+already in MXFP4 form, so that the oracle needs no quantizer pass over billions
+of values: :func:`random_mxfp4_operands` draws every code byte uniformly (both
+nibbles, all sixteen E2M1 codes, signed zero included) and every E8M0 scale byte
+uniformly from a narrow band around 127, in the order Q codes, Q scales, K
+codes, K scales, Vt codes, Vt scales.
 """
 import math
 from dataclasses import dataclass
@@ -127,3 +134,21 @@ def sampled_rows(w, n=N_SAMPLED_ROWS):
 def as_f64(t):
     """fp64 NumPy copy of a CPU tensor (bf16 widens exactly)."""
     return t.detach().to(torch.float64).cpu().numpy()
+
+
+def random_mxfp4_operands(B, H, N, d, seed, scale_lo=125, scale_hi=129):
+    """Uniform random MXFP4 operand bytes in the layout of the forward's
+    arguments: q/k codes [B, H, N, d/2] and scales [B, H, N, d/32], Vt codes
+    [B, H, d, N/2] and scales [B, H, d, N/32] (uint8 CPU tensors).
+
+    Scale bytes lie in [scale_lo, scale_hi]; with a band of width 4 every score
+    of d <= 128 products is a multiple of 2^-6 below 2^17, so it is exact in fp32.
+    """
+    g = torch.Generator().manual_seed(seed)
+
+    def draw(shape, lo, hi):
+        return torch.randint(lo, hi + 1, shape, generator=g, dtype=torch.uint8)
+
+    return (draw((B, H, N, d // 2), 0, 255), draw((B, H, N, d // 32), scale_lo, scale_hi),
+            draw((B, H, N, d // 2), 0, 255), draw((B, H, N, d // 32), scale_lo, scale_hi),
+            draw((B, H, d, N // 2), 0, 255), draw((B, H, d, N // 32), scale_lo, scale_hi))
