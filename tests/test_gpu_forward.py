@@ -97,7 +97,7 @@ def test_full_size_sampled_rows(fa, name):
     _run_and_check(fa, host64, dev, workloads.sampled_rows(name), name)
 
 
-def _check_byte_operands(fa, ops_cpu, rows, label):
+def _check_byte_operands(fa, ops_cpu, rows, label, causal=False):
     """Forward and Direct-P dump of MXFP4 operand bytes against the oracle on the
     flattened query ``rows`` (the same bytes feed both sides)."""
     from oracle import directp
@@ -108,8 +108,8 @@ def _check_byte_operands(fa, ops_cpu, rows, label):
     print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)}: GPU launches", flush=True)
     ops = tuple(t.cuda() for t in ops_cpu)
     row_ids = torch.from_numpy(rows).cuda()
-    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s)
-    out = fa.forward_mxfp4(*ops, softmax_scale=s)
+    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, causal=causal)
+    out = fa.forward_mxfp4(*ops, softmax_scale=s, causal=causal)
     torch.cuda.synchronize()
     assert torch.equal(out, dump["out"]), f"{label}: debug launch output differs from the forward"
     assert bool(torch.isfinite(out).all()), f"{label}: non-finite output"
@@ -122,7 +122,7 @@ def _check_byte_operands(fa, ops_cpu, rows, label):
     for bh in np.unique(rows // N):
         b, h = divmod(int(bh), H)
         sel = np.nonzero(rows // N == bh)[0]
-        res = directp.forward_rows(*(t[b, h].numpy() for t in ops_cpu), rows[sel] % N, s)
+        res = directp.forward_rows(*(t[b, h].numpy() for t in ops_cpu), rows[sel] % N, s, causal=causal)
         for key in ref:
             ref[key].append(res[key])
         order.append(sel)
@@ -134,7 +134,8 @@ def _check_byte_operands(fa, ops_cpu, rows, label):
     assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{label}: rel {rel} cos {cos}"
 
 
-def test_longest_sequence_sampled_rows(fa):
+@pytest.mark.parametrize("causal", [False, True])
+def test_longest_sequence_sampled_rows(fa, causal):
     """N = 2^22 keys, the largest the entry point accepts: every byte offset within
     the head near its 32-bit limit, 32768 key tiles per workgroup.  Rows: the first
     and last of the sequence, of a query tile and of a workgroup, and random ones."""
@@ -142,7 +143,7 @@ def test_longest_sequence_sampled_rows(fa):
     ops_cpu = workloads.random_mxfp4_operands(1, 1, N, 128, seed=22)
     rows = np.unique(np.concatenate([[0, 1, 255, 256, N // 2 + 31, N - 257, N - 256, N - 1],
                                      np.random.default_rng(22).integers(0, N, 8)]))
-    _check_byte_operands(fa, ops_cpu, rows, "N=2^22")
+    _check_byte_operands(fa, ops_cpu, rows, f"N=2^22 causal={causal}", causal=causal)
 
 
 def test_largest_grid_sampled_rows(fa):
