@@ -22,6 +22,21 @@ def _stream(t):
     return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
 
 
+def _same_device(*tensors):
+    """The one device every tensor of a call lives on (the library launches on the
+    current HIP device, so each call runs with that device made current)."""
+    dev = tensors[0].device
+    for t in tensors[1:]:
+        if t.device != dev:
+            raise ValueError(f"tensors of one call must share a device: {dev} and {t.device}")
+    return dev
+
+
+def _launch(device, fn, *args):
+    with torch.cuda.device(device):
+        check(fn(*args))
+
+
 def _need(t, name, dtype=None, ndim=None):
     if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
         raise ValueError(f"{name} must be a GPU tensor")
@@ -55,11 +70,11 @@ def quantize_mxfp4(x, axis=-1, n_anchor=0):
     codes = torch.empty(cshape, dtype=torch.uint8, device=x.device)
     scales = torch.empty(sshape, dtype=torch.uint8, device=x.device)
     if n_anchor:
-        check(lib.fp4attn_quantize_mxfp4_anchored(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, n_anchor,
-                                                  _ptr(codes), _ptr(scales), _stream(x)))
+        _launch(x.device, lib.fp4attn_quantize_mxfp4_anchored, _ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis,
+                n_anchor, _ptr(codes), _ptr(scales), _stream(x))
     else:
-        check(lib.fp4attn_quantize_mxfp4(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, _ptr(codes),
-                                         _ptr(scales), _stream(x)))
+        _launch(x.device, lib.fp4attn_quantize_mxfp4, _ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis,
+                _ptr(codes), _ptr(scales), _stream(x))
     return codes, scales
 
 
@@ -80,8 +95,8 @@ def quantize_mxfp8(x, axis=-1):
         raise ValueError("axis must be -1 or -2")
     codes = torch.empty(cshape, dtype=torch.uint8, device=x.device)
     scales = torch.empty(sshape, dtype=torch.uint8, device=x.device)
-    check(lib.fp4attn_quantize_mxfp8(_ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, _ptr(codes),
-                                     _ptr(scales), _stream(x)))
+    _launch(x.device, lib.fp4attn_quantize_mxfp8, _ptr(x), _DTYPES[x.dtype], batch, rows, cols, c_axis, _ptr(codes),
+            _ptr(scales), _stream(x))
     return codes, scales
 
 
@@ -159,16 +174,17 @@ def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, sof
     ops = (q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales)
     _check_operands(B, H, N, d, ops, pv_fp8)
     out = _out(out, B, H, N, d, out_dtype, q_codes.device)
+    dev = _same_device(*ops, out, *(() if lse is None else (lse,)))
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
     if ex2_pairs is None and guard is None and not causal and lse is None and not pv_fp8:
-        check(lib.fp4attn_forward_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
-                                        _DTYPES[out.dtype], _stream(out)))
+        _launch(dev, lib.fp4attn_forward_mxfp4, *(_ptr(t) for t in ops), B, H, N, d, s, affine_a, affine_b, _ptr(out),
+                _DTYPES[out.dtype], _stream(out))
     else:
         if lse is not None and tuple(lse.shape) != (B, H, N):
             raise ValueError(f"lse has shape {tuple(lse.shape)}, expected {(B, H, N)}")
         o = forward_options(affine_a, affine_b, ex2_pairs or 0, guard, causal, lse, pv_fp8)
-        check(lib.fp4attn_forward_mxfp4_ex(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
-                                           _DTYPES[out.dtype], _stream(out)))
+        _launch(dev, lib.fp4attn_forward_mxfp4_ex, *(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o),
+                _ptr(out), _DTYPES[out.dtype], _stream(out))
     return out
 
 
@@ -188,7 +204,7 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
     _check_operands(B, H, N, d, ops, pv_fp8)
     _need(row_ids, "row_ids", torch.int64, 1)
     R = row_ids.numel()   # 0: no dump, the launch is the plain forward kernel
-    dev = q_codes.device
+    dev = _same_device(*ops, row_ids)
     out = torch.empty((B, H, N, d), dtype=out_dtype, device=dev)
     res = {
         "out": out,
@@ -203,10 +219,10 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
         res["lse"] = torch.empty((B, H, N), dtype=torch.float32, device=dev)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
     o = forward_options(affine_a, affine_b, ex2_pairs, guard, causal, res.get("lse"), pv_fp8)
-    check(lib.fp4attn_debug_directp_mxfp4(*(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o), _ptr(out),
-                                          _DTYPES[out_dtype], _ptr(row_ids) if R else None, R, _ptr(res["p_codes"]),
-                                          _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),
-                                          _ptr(res["wg_clock"]) if wg_clock else None, _stream(out)))
+    _launch(dev, lib.fp4attn_debug_directp_mxfp4, *(_ptr(t) for t in ops), B, H, N, d, s, ctypes.byref(o),
+            _ptr(out), _DTYPES[out_dtype], _ptr(row_ids) if R else None, R, _ptr(res["p_codes"]),
+            _ptr(res["block_exp"]), _ptr(res["row_m"]), _ptr(res["row_d"]),
+            _ptr(res["wg_clock"]) if wg_clock else None, _stream(out))
     return res
 
 
@@ -216,7 +232,8 @@ def transpose_bf16(v):
     lead = tuple(v.shape[:-2])
     rows, cols = v.shape[-2:]
     vt = torch.empty(lead + (cols, rows), dtype=torch.bfloat16, device=v.device)
-    check(lib.fp4attn_transpose_bf16(_ptr(v), math.prod(lead) if lead else 1, rows, cols, _ptr(vt), _stream(v)))
+    _launch(v.device, lib.fp4attn_transpose_bf16, _ptr(v), math.prod(lead) if lead else 1, rows, cols, _ptr(vt),
+            _stream(v))
     return vt
 
 
@@ -229,7 +246,8 @@ def forward_bf16(q, k, vt, softmax_scale=None, out=None, out_dtype=torch.float32
     if tuple(k.shape) != (B, H, N, d) or tuple(vt.shape) != (B, H, d, N):
         raise ValueError("k must be [B, H, N, d] and vt [B, H, d, N]")
     out = _out(out, B, H, N, d, out_dtype, q.device)
+    dev = _same_device(q, k, vt, out)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    check(lib.fp4attn_forward_bf16(_ptr(q), _ptr(k), _ptr(vt), B, H, N, d, s, _ptr(out), _DTYPES[out.dtype],
-                                   _stream(out)))
+    _launch(dev, lib.fp4attn_forward_bf16, _ptr(q), _ptr(k), _ptr(vt), B, H, N, d, s, _ptr(out), _DTYPES[out.dtype],
+            _stream(out))
     return out

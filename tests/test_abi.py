@@ -139,3 +139,14 @@ def test_forward_options(lib):
     o.affine_a = 1.5
     assert e(*FAKE[:6], 1, 1, 128, 80, 0.125, ctypes.byref(o), FAKE[6], 0, None) == 2     # d = 80
     assert e(None, *FAKE[1:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, None) == 1
+
+
+def test_binding_requires_one_device_per_call():
+    """The binding runs each call with the operands' device current; operands on
+    two devices are refused before anything reaches the library."""
+    import torch
+    from paper_2609_04105_amd import api
+    a, b = torch.zeros(2), torch.zeros(2, device="meta")
+    assert api._same_device(a, a) == a.device
+    with pytest.raises(ValueError, match="share a device"):
+        api._same_device(a, a, b)
