@@ -15,7 +15,9 @@
  * ---------------------------------------
  * - Tensor pointers are DEVICE pointers owned by the caller; the library never
  *   allocates, frees or keeps them.  Every pointer must be 16-byte aligned.
- * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream of
+ *   the current device).  The work runs on the device that `stream` belongs
+ *   to, and every pointer must be memory of that device (or mapped into it).
  *   Arguments are validated synchronously on the host; on success the work is
  *   enqueued asynchronously on `stream` and the call returns without waiting.
  *   On any error nothing is enqueued and the outputs are untouched.
