@@ -9,8 +9,8 @@ import pytest
 import torch
 
 import workloads
-from parity import (O_COS_MIN, O_REL_L2_MAX, check_directp_dump, gpu_operands, load_workload, oracle_rows,
-                    rel_l2_cos)
+from parity import (O_COS_MIN, O_REL_L2_MAX, check_directp_dump, check_fp8_dump, check_guarded_dump, gpu_operands,
+                    load_workload, oracle_rows, rel_l2_cos)
 
 pytestmark = pytest.mark.gpu
 
@@ -97,10 +97,12 @@ def test_full_size_sampled_rows(fa, name):
     _run_and_check(fa, host64, dev, workloads.sampled_rows(name), name)
 
 
-def _check_byte_operands(fa, ops_cpu, rows, label, causal=False):
+def _check_byte_operands(fa, ops_cpu, rows, label, causal=False, guard=None, pv_fp8=False):
     """Forward and Direct-P dump of MXFP4 operand bytes against the oracle on the
-    flattened query ``rows`` (the same bytes feed both sides)."""
-    from oracle import directp
+    flattened query ``rows`` (the same bytes feed both sides; with ``guard`` the
+    key order of the bytes is the anchor order)."""
+    from oracle import directp, fp8pv
+    from oracle import guard as guard_oracle
     B, H, N, half_d = ops_cpu[0].shape
     d = 2 * half_d
     s = 1.0 / np.sqrt(d)
@@ -108,8 +110,8 @@ def _check_byte_operands(fa, ops_cpu, rows, label, causal=False):
     print(f"[{label}] B{B} H{H} N{N} d{d} rows={len(rows)}: GPU launches", flush=True)
     ops = tuple(t.cuda() for t in ops_cpu)
     row_ids = torch.from_numpy(rows).cuda()
-    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, causal=causal)
-    out = fa.forward_mxfp4(*ops, softmax_scale=s, causal=causal)
+    dump = fa.debug_directp_mxfp4(*ops, row_ids, softmax_scale=s, causal=causal, guard=guard, pv_fp8=pv_fp8)
+    out = fa.forward_mxfp4(*ops, softmax_scale=s, causal=causal, guard=guard, pv_fp8=pv_fp8)
     torch.cuda.synchronize()
     assert torch.equal(out, dump["out"]), f"{label}: debug launch output differs from the forward"
     assert bool(torch.isfinite(out).all()), f"{label}: non-finite output"
@@ -117,18 +119,30 @@ def _check_byte_operands(fa, ops_cpu, rows, label, causal=False):
     del ops, out
     dump = {key: val for key, val in dump.items() if key != "out"}
     print(f"[{label}] oracle", flush=True)
-    ref = {"O": [], "E": [], "M": [], "D": [], "codes": []}
+    keys = ("O", "ebar", "D", "codes") if guard else ("O", "E", "M", "D", "codes")
+    ref = {key: [] for key in keys}
     order = []
     for bh in np.unique(rows // N):
         b, h = divmod(int(bh), H)
         sel = np.nonzero(rows // N == bh)[0]
-        res = directp.forward_rows(*(t[b, h].numpy() for t in ops_cpu), rows[sel] % N, s, causal=causal)
+        head = [t[b, h].numpy() for t in ops_cpu]
+        if guard:
+            res = guard_oracle.forward_rows(*head, rows[sel] % N, s, *guard)
+        elif pv_fp8:
+            res = fp8pv.forward_rows(*head, rows[sel] % N, s, causal=causal)
+        else:
+            res = directp.forward_rows(*head, rows[sel] % N, s, causal=causal)
         for key in ref:
             ref[key].append(res[key])
         order.append(sel)
     order = np.concatenate(order)
     ref = {key: np.concatenate(val)[np.argsort(order)] for key, val in ref.items()}
-    mismatch = check_directp_dump(dump, ref, label)
+    if guard:
+        mismatch = check_guarded_dump(dump, ref, label)
+    elif pv_fp8:
+        mismatch = check_fp8_dump(dump, ref, label)
+    else:
+        mismatch = check_directp_dump(dump, ref, label)
     rel, cos = rel_l2_cos(got, ref["O"])
     print(f"[{label}] code mismatch {mismatch:.2e}  O rel-L2 {rel:.3e}  cos {cos:.8f}", flush=True)
     assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{label}: rel {rel} cos {cos}"
@@ -144,6 +158,19 @@ def test_longest_sequence_sampled_rows(fa, causal):
     rows = np.unique(np.concatenate([[0, 1, 255, 256, N // 2 + 31, N - 257, N - 256, N - 1],
                                      np.random.default_rng(22).integers(0, N, 8)]))
     _check_byte_operands(fa, ops_cpu, rows, f"N=2^22 causal={causal}", causal=causal)
+
+
+@pytest.mark.parametrize("route", ["guard_110_16", "fp8_pv"])
+def test_longest_sequence_other_routes(fa, route):
+    """N = 2^22 on the sampled guard (the paper's margin and shift; the bytes'
+    first 128 keys are the anchors) and on the FP8 P/V route (Vt 2^22 bytes per
+    row of d)."""
+    N = 1 << 22
+    pv_fp8 = route == "fp8_pv"
+    ops_cpu = workloads.random_mxfp4_operands(1, 1, N, 128, seed=23, v_fp8=pv_fp8)
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, N // 2 + 31, N - 257, N - 256, N - 1],
+                                     np.random.default_rng(23).integers(0, N, 8)]))
+    _check_byte_operands(fa, ops_cpu, rows, f"N=2^22 {route}", guard=None if pv_fp8 else (110, 16), pv_fp8=pv_fp8)
 
 
 def test_largest_grid_sampled_rows(fa):

@@ -71,3 +71,13 @@ def test_random_mxfp4_operand_scores_are_exact_in_fp32():
         k6 = mxfp4.scaled_operand(big, np.full((2, 4), sk, dtype=np.uint8))
         raw = directp.raw_scores(q6, k6)
         assert np.all(raw == 128 * 36.0 * 2.0 ** (sq + sk - 254))
+
+
+def test_random_mxfp8_vt_bytes_are_finite_e4m3():
+    ops = workloads.random_mxfp4_operands(1, 2, 256, 64, seed=7, v_fp8=True)
+    vt = ops[4]
+    assert tuple(vt.shape) == (1, 2, 64, 256) and tuple(ops[5].shape) == (1, 2, 64, 8)
+    assert int((vt & 0x7F).max()) == 0x7E          # 0x7f / 0xff (NaN) never drawn
+    assert int((vt >> 7).min()) == 0 and int((vt >> 7).max()) == 1
+    from oracle import fp8pv
+    assert np.all(np.isfinite(fp8pv.dequantize(vt[0, 0].numpy(), ops[5][0, 0].numpy())))

@@ -136,19 +136,27 @@ def as_f64(t):
     return t.detach().to(torch.float64).cpu().numpy()
 
 
-def random_mxfp4_operands(B, H, N, d, seed, scale_lo=125, scale_hi=129):
+def random_mxfp4_operands(B, H, N, d, seed, scale_lo=125, scale_hi=129, v_fp8=False):
     """Uniform random MXFP4 operand bytes in the layout of the forward's
     arguments: q/k codes [B, H, N, d/2] and scales [B, H, N, d/32], Vt codes
     [B, H, d, N/2] and scales [B, H, d, N/32] (uint8 CPU tensors).
 
     Scale bytes lie in [scale_lo, scale_hi]; with a band of width 4 every score
     of d <= 128 products is a multiple of 2^-6 below 2^17, so it is exact in fp32.
+    ``v_fp8``: Vt codes are E4M3 bytes [B, H, d, N] instead, a uniform sign bit
+    over a magnitude byte uniform in [0, 0x7e] (every finite E4M3 value; 0x7f
+    is NaN).
     """
     g = torch.Generator().manual_seed(seed)
 
     def draw(shape, lo, hi):
         return torch.randint(lo, hi + 1, shape, generator=g, dtype=torch.uint8)
 
-    return (draw((B, H, N, d // 2), 0, 255), draw((B, H, N, d // 32), scale_lo, scale_hi),
-            draw((B, H, N, d // 2), 0, 255), draw((B, H, N, d // 32), scale_lo, scale_hi),
-            draw((B, H, d, N // 2), 0, 255), draw((B, H, d, N // 32), scale_lo, scale_hi))
+    ops = [draw((B, H, N, d // 2), 0, 255), draw((B, H, N, d // 32), scale_lo, scale_hi),
+           draw((B, H, N, d // 2), 0, 255), draw((B, H, N, d // 32), scale_lo, scale_hi)]
+    if v_fp8:
+        ops.append(draw((B, H, d, N), 0, 0x7E) | (draw((B, H, d, N), 0, 1) << 7))
+    else:
+        ops.append(draw((B, H, d, N // 2), 0, 255))
+    ops.append(draw((B, H, d, N // 32), scale_lo, scale_hi))
+    return tuple(ops)
