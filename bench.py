@@ -12,7 +12,9 @@ ops count 4 B H N^2 d per step (eq. hao-flops) over the step time.
 Prints one JSON line.  Also reported: the same-design BF16 kernel on the same
 inputs (windows interleaved with the FP4 ones, the paper's speedup
 t_BF16 / t_FP4), the roofline of the forward kernel against the dense MXFP4
-matrix peak, and the CPU oracle timed on a bounded sample of rows.  The
+matrix peak (and, beside it, the shader clock the kernel ran at and the rate
+a stream of FP4 matrix products alone sustains on the workload's K and Q
+codes), and the CPU oracle timed on a bounded sample of rows.  The
 defaults follow the paper's timing protocol (Sec. "Operator benchmark suites"): 240
 warmup steps (over 300 ms), 2200 timed steps (about 3 s), and ten interleaved
 300 ms windows of each of the FP4 and BF16 kernels.
@@ -162,6 +164,24 @@ def measured_clock_ghz(torch, fa, ops, w, launches=5):
     return cyc / (ticks / 100e6) / 1e9
 
 
+def sustained_mfma_tflops(torch, fa, a_codes, b_codes, blocks=1024, iters=100000, launches=7):
+    """Rate of a stream of FP4 32x32x64 matrix products with nothing else running,
+    on operand bytes of the workload (the QK product's K and Q codes): the matrix
+    unit's sustained ceiling on this board for this data, beside the spec peak.
+    Median over ``launches`` after one warmup launch."""
+    times = []
+    for i in range(launches + 1):
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        _, flop = fa.debug_mfma_stream(a_codes, b_codes, blocks, iters)
+        end.record()
+        torch.cuda.synchronize()
+        if i:
+            times.append(start.elapsed_time(end))
+    ms = sorted(times)[len(times) // 2]
+    return flop / (ms * 1e-3) / 1e12
+
+
 def cpu_oracle_baseline(w, q, k, v, budget_s=12.0):
     """Time the oracle (as it stands) on consecutive rows of head (0, 0) of the bench
     inputs (CPU tensors q, k, v [B, H, N, d]) until the budget is spent.  Returns the
@@ -309,6 +329,9 @@ def main():
     traffic = _traffic()
     clk = measured_clock_ghz(torch, fa, ops, w)
     peak_clk = MXFP4_PEAK_TFLOPS * clk / SPEC_CLOCK_GHZ
+    stream_blocks = min(1024, ops[0].numel() // (256 * 64))  # 64 operand bytes per thread
+    stream = sustained_mfma_tflops(torch, fa, ops[2].reshape(-1), ops[0].reshape(-1), blocks=stream_blocks) \
+        if stream_blocks >= 1 else None
     roof = {
         "bound": "mfma",
         "achieved": round(tflops, 2),
@@ -320,6 +343,8 @@ def main():
         "measured_clock_ghz": round(clk, 3),
         "peak_at_measured_clock": round(peak_clk, 1),
         "frac_at_measured_clock": round(tflops / peak_clk, 4),
+        "sustained_mfma_stream": round(stream, 1) if stream else None,
+        "frac_of_sustained_mfma_stream": round(tflops / stream, 4) if stream else None,
         "algorithmic_flops_per_launch": flops,
     }
     line = {

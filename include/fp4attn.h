@@ -299,6 +299,22 @@ fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t
                                            int32_t* row_m, float* row_d, uint64_t* wg_clock,
                                            void* stream);
 
+/*
+ * Measurement hook: the sustained rate of the scaled FP4 matrix unit on given
+ * operands, the ceiling the forward's two products are compared against.
+ * Launches `blocks` x 256 threads; thread t keeps the four 16-byte fragments
+ * a_codes[64 t, 64 t + 64) and the four b_codes[64 t, 64 t + 64) (E2M1 codes,
+ * two per byte) in registers, issues `iters` rounds of four independent
+ * 32x32x64 FP4 products with E8M0 scale bytes 127 (fragment i of A with
+ * fragment (i + 1) % 4 of B), and writes the sum of its sixteen-element
+ * accumulators to out[t].  Work: blocks * 256 / 64 waves * iters * 4 products
+ * of 2 * 32 * 32 * 64 flop.  a_codes and b_codes hold blocks * 256 * 64
+ * bytes each, out blocks * 256 floats.  Errors: INVALID_ARG for null or
+ * misaligned pointers, blocks outside [1, 65535], iters < 1.
+ */
+fp4attn_status fp4attn_debug_mfma_stream(const uint8_t* a_codes, const uint8_t* b_codes, int blocks, int iters,
+                                         float* out, void* stream);
+
 /* Static description of a status code; never NULL. */
 const char* fp4attn_status_string(int status);
 

@@ -16,6 +16,7 @@ from ._lib import (  # noqa: F401
 )
 from .api import (  # noqa: F401
     debug_directp_mxfp4,
+    debug_mfma_stream,
     forward_bf16,
     forward_mxfp4,
     forward_options,

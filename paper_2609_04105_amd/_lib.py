@@ -34,6 +34,7 @@ SIGNATURES = {
     "fp4attn_forward_mxfp4_ex": [_c_p] * 6 + [_i64] * 4 + [_f32, ctypes.POINTER(ForwardOptions), _c_p, _int, _c_p],
     "fp4attn_debug_directp_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32, ctypes.POINTER(ForwardOptions)]
     + [_c_p, _int, _c_p, _i64] + [_c_p] * 5 + [_c_p],
+    "fp4attn_debug_mfma_stream": [_c_p, _c_p, _int, _int, _c_p, _c_p],
     "fp4attn_status_string": [_int],
     "fp4attn_last_error": [],
     "fp4attn_abi_version": [],

@@ -226,6 +226,22 @@ def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scale
     return res
 
 
+def debug_mfma_stream(a_codes, b_codes, blocks, iters):
+    """Sustained FP4 matrix-unit stream on given operands (fp4attn_debug_mfma_stream):
+    ``blocks`` x 256 threads, each with 64 bytes of ``a_codes`` and of ``b_codes``
+    (uint8, at least blocks * 256 * 64 bytes each); returns the per-thread
+    accumulator sums [blocks * 256] fp32 and the flop count of the launch."""
+    need = blocks * 256 * 64
+    for t, name in ((a_codes, "a_codes"), (b_codes, "b_codes")):
+        _need(t, name, torch.uint8)
+        if t.numel() < need:
+            raise ValueError(f"{name} holds {t.numel()} bytes, the launch reads {need}")
+    dev = _same_device(a_codes, b_codes)
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+    _launch(dev, lib.fp4attn_debug_mfma_stream, _ptr(a_codes), _ptr(b_codes), blocks, iters, _ptr(out), _stream(out))
+    return out, blocks * 4 * iters * 4 * 2.0 * 32 * 32 * 64
+
+
 def transpose_bf16(v):
     """V [..., N, d] bf16 -> V^T [..., d, N] (layout preparation of the BF16 baseline)."""
     _need(v, "v", torch.bfloat16)

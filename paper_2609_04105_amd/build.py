@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libfp4attn.so")
 SOURCES = ["fwd_mxfp4_guard.hip", "fwd_mxfp4_causal.hip", "fwd_mxfp4_ex2.hip", "fwd_mxfp4.hip",
-           "fwd_mxfp4_ex2_dense.hip", "fwd_mxfp4_fp8pv.hip", "fwd_bf16.hip", "api.hip", "quantize.hip"]
+           "fwd_mxfp4_ex2_dense.hip", "fwd_mxfp4_fp8pv.hip", "fwd_bf16.hip", "api.hip", "quantize.hip", "mfma_stream.hip"]
 # The attention kernels never rely on NaN ordering in fmax; without this flag the
 # compiler canonicalizes every fmax operand with an extra v_max_f32.
 EXTRA = {f: ["-fno-honor-nans"] for f in ("fwd_mxfp4.hip", "fwd_mxfp4_ex2.hip", "fwd_mxfp4_ex2_dense.hip",

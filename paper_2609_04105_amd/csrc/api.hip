@@ -184,6 +184,11 @@ fp4attn_status quantize_common(const void* src, int src_dtype, int64_t batch, in
 
 }  // namespace
 
+namespace fp4attn {
+// mfma_stream.hip: blocks x 256 threads; a and b hold 64 bytes per thread, out one float per thread.
+hipError_t launch_mfma_stream(const void* a, const void* b, int blocks, int iters, float* out, hipStream_t stream);
+}  // namespace fp4attn
+
 extern "C" {
 
 fp4attn_status fp4attn_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols,
@@ -308,6 +313,17 @@ fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t ro
                   "transpose launch");
 }
 
+fp4attn_status fp4attn_debug_mfma_stream(const uint8_t* a_codes, const uint8_t* b_codes, int blocks, int iters,
+                                         float* out, void* stream) {
+  REQUIRE_PTR(a_codes);
+  REQUIRE_PTR(b_codes);
+  REQUIRE_PTR(out);
+  if (blocks < 1 || blocks > 65535 || iters < 1)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "blocks must be in [1, 65535] and iters >= 1");
+  return from_hip(fp4attn::launch_mfma_stream(a_codes, b_codes, blocks, iters, out, static_cast<hipStream_t>(stream)),
+                  "mfma stream launch");
+}
+
 const char* fp4attn_status_string(int status) {
   switch (status) {
     case FP4ATTN_OK: return "ok";
@@ -320,6 +336,6 @@ const char* fp4attn_status_string(int status) {
 
 const char* fp4attn_last_error(void) { return g_last_error; }
 
-int fp4attn_abi_version(void) { return (1 << 16) | 3; }
+int fp4attn_abi_version(void) { return (1 << 16) | 4; }
 
 }  // extern "C"

@@ -90,6 +90,12 @@ def test_quantize_and_bf16_validation(lib):
     assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, FAKE[7], -1, *FAKE[:4], None, None) == 1  # n_rows < 0
     assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, FAKE[7], 1, *FAKE[:4], ctypes.c_void_p(4096 + 8),
              None) == 1                                                 # misaligned wg_clock
+    m = lib.fp4attn_debug_mfma_stream
+    assert m(FAKE[0], FAKE[1], 0, 10, FAKE[2], None) == 1              # blocks < 1
+    assert m(FAKE[0], FAKE[1], 65536, 10, FAKE[2], None) == 1          # blocks > 65535
+    assert m(FAKE[0], FAKE[1], 4, 0, FAKE[2], None) == 1               # iters < 1
+    assert m(None, FAKE[1], 4, 10, FAKE[2], None) == 1
+    assert m(FAKE[0], FAKE[1], 4, 10, ctypes.c_void_p(4100), None) == 1  # misaligned out
 
 
 def test_forward_options(lib):
