@@ -184,6 +184,43 @@ def test_largest_grid_sampled_rows(fa):
     _check_byte_operands(fa, ops_cpu, rows, f"B{B} H{H}")
 
 
+def test_concurrent_threads_and_streams(fa):
+    """No state is shared between calls: two host threads, each enqueueing
+    forwards on its own stream (default priority), reproduce the sequential
+    outputs bit for bit."""
+    import threading
+    g = torch.Generator().manual_seed(31)
+    shapes = [(1, 4, 1024, 128), (2, 3, 512, 64)]
+    cases = []
+    for shape in shapes:
+        q, k, v = (torch.randn(*shape, generator=g).to(torch.bfloat16).cuda() for _ in range(3))
+        ops = fa.quantize_qkv(q, k, v)
+        cases.append((ops, fa.forward_mxfp4(*ops), fa.forward_mxfp4(*ops, causal=True)))
+    torch.cuda.synchronize()
+    results, errors = {}, []
+
+    def worker(i):
+        try:
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                ops = cases[i][0]
+                outs = [(fa.forward_mxfp4(*ops), fa.forward_mxfp4(*ops, causal=True)) for _ in range(4)]
+            stream.synchronize()
+            results[i] = outs
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(cases))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for i, (_, ref, ref_causal) in enumerate(cases):
+        for out, out_causal in results[i]:
+            assert torch.equal(out, ref) and torch.equal(out_causal, ref_causal)
+
+
 def test_affine_variant_and_scale(fa):
     """The Wan fit (A, B) = (1.6, 0.95) and a non-default softmax scale."""
     host64, dev = load_workload("small_b1h8_n1024_d64", H=2)
