@@ -130,83 +130,104 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_kernel(const T* __restrict
 }
 
 // bf16 fast path of the same rule, exact in 32-bit arithmetic.  A bf16 value
-// has at most 8 significant bits, so s = |v| / 2^e_ceil (<= 1) and r = 6 s are
-// exact in fp32, and the hardware converter's E2M1 rounding (nearest, ties to
-// the even code, saturating at 6) gives qc = E2M1(r) and qf = E2M1(min(2r, 6))
-// exactly; the decode instruction returns their values.  A term
-// A B = (2 qc - qf)(4 r - qf - 2 qc) is nonzero only for r > 1/8, where r is a
-// multiple of 2^-12, so each term is exact in fp32 and 4096 A B is an integer
-// below 2^21; the sum of 32 of them is exact in int32.  The codes of the chosen
-// amplitude are the ones already converted (unless the E8M0 range clamps it).
+// has at most 8 significant bits, so r = 6 v / 2^e_ceil has at most 10 and is
+// exact in fp32; the hardware converter's E2M1 rounding (nearest, ties to the
+// even code, saturating at 6) gives qc = E2M1(r) and qf = E2M1(2 r) exactly and
+// the decode instruction returns their values, so the rule's sum is evaluated
+// exactly (see below).  The codes of the chosen amplitude are the ones already
+// converted (unless the E8M0 range clamps it).
 //   raw[i]: elements 2i (bits 0-15) and 2i + 1 (bits 16-31).  Returns the E8M0
 //   byte; codes[j] holds elements 8 j .. 8 j + 7, even element in the low nibble.
 __device__ __forceinline__ unsigned mxfp4_block_bf16(const unsigned (&raw)[16], unsigned (&codes)[4]) {
-  float mag[32];
-  unsigned nonfinite = 0, sign[4] = {0u, 0u, 0u, 0u};
+  // Block maximum on the magnitude bits, two bf16 values per packed 16-bit max:
+  // magnitudes order as their bit patterns, and Inf and NaN sort above every
+  // finite value.
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  u16x2 mx = {0, 0};
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const unsigned w = raw[i];
-    mag[2 * i] = __builtin_bit_cast(float, (w << 16) & 0x7fff0000u);
-    mag[2 * i + 1] = __builtin_bit_cast(float, w & 0x7fff0000u);
-    nonfinite |= ((w & 0x7f80u) == 0x7f80u) | ((w & 0x7f800000u) == 0x7f800000u);
-    // sign bits to code bit 3 of the even element's nibble and bit 7 of the odd one's
-    sign[i / 4] |= (((w >> 12) & 0x8u) | ((w >> 24) & 0x80u)) << (8 * (i % 4));
-  }
-  if (nonfinite) {
+  for (int i = 0; i < 16; ++i) mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2, raw[i] & 0x7fff7fffu));
+  const unsigned amax_bits = mx[0] > mx[1] ? mx[0] : mx[1];
+  if (amax_bits >= 0x7f80u) {  // a NaN or an infinity in the block
 #pragma unroll
     for (int j = 0; j < 4; ++j) codes[j] = 0u;
     return 255u;
   }
-  float amax = 0.0f;
+  // Signed values go straight into the converter: its codes carry the input's
+  // sign bit (-0.0 and negative values that round to zero give 0x8).
+  // encode: the codes of 6 v / 2^e, scaled in two exact steps (valid for every
+  // E8M0 exponent, where the single factor 6 / 2^e may overflow).
+  auto encode = [&](int e, unsigned (&w)[4]) {
 #pragma unroll
-  for (int j = 0; j < 32; ++j) amax = fmaxf(amax, mag[j]);
-  if (amax == 0.0f) {  // zero block: byte 0, code magnitudes 0, signs kept
-#pragma unroll
-    for (int j = 0; j < 4; ++j) codes[j] = sign[j];
+    for (int j = 0; j < 4; ++j) {
+      unsigned acc = 0u;
+      static_for<4>([&](auto P_) {
+        constexpr int pb = decltype(P_)::value;
+        const unsigned word = raw[4 * j + pb];
+        const float v0 = __builtin_bit_cast(float, word << 16), v1 = __builtin_bit_cast(float, word & 0xffff0000u);
+        acc = cvt_pk_fp4<pb>(pb == 0 ? 0u : acc, 6.0f * ldexpf(v0, -e), 6.0f * ldexpf(v1, -e), 1.0f);
+      });
+      w[j] = acc;
+    }
+  };
+  if (amax_bits == 0u) {  // zero block: byte 0, every code a signed zero
+    encode(0, codes);
     return 0u;
   }
   int x;
-  const float m = frexpf(amax, &x);  // amax = m 2^x, m in [0.5, 1)
+  const float m = frexpf(__builtin_bit_cast(float, amax_bits << 16), &x);  // amax = m 2^x, m in [0.5, 1)
   const int e_floor = x - 1, e_ceil = (m == 0.5f) ? x - 1 : x;
+  // r = 6 v / 2^e_ceil (one exact multiply), qc = E2M1(r) and qf = E2M1(2 r)
+  // (the converter divides by its scale operand and saturates at 6).  The
+  // choice compares 4 sum(a r) with sum(a b), a = 2 qc - qf, b = 2 qc + qf: the
+  // floor amplitude wins iff sum a (4 r - b) < 0.  Only values with |r| >= 1/8
+  // have a != 0; such r are multiples of 2^-12, and |a| <= qc <= 6 because
+  // qf >= qc, so both sums are exact in fp32 (multiples of 2^-13 below 2^11, and
+  // of 2^-2 below 2^12).
+  // The single factor 6 / 2^e_ceil is finite for e_ceil >= -125; blocks below
+  // that (amax under 2^-125) take the two-step scaling of encode.
+  const float sc = ldexpf(6.0f, -e_ceil);
   unsigned cc[4], cf[4];
-  int delta = 0;
+  float s_ar = 0.0f, s_ab = 0.0f;
+  auto convert = [&](auto TWO_STEP_) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    unsigned wc = 0u, wf = 0u;
-    static_for<4>([&](auto P_) {
-      constexpr int pb = decltype(P_)::value;
-      const int k = 8 * j + 2 * pb;
-      const float r0 = 6.0f * ldexpf(mag[k], -e_ceil), r1 = 6.0f * ldexpf(mag[k + 1], -e_ceil);
-      wc = cvt_pk_fp4<pb>(pb == 0 ? 0u : wc, r0, r1, 1.0f);
-      wf = cvt_pk_fp4<pb>(pb == 0 ? 0u : wf, fminf(2.0f * r0, 6.0f), fminf(2.0f * r1, 6.0f), 1.0f);
-      const v2f qc = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wc, 1.0f, pb);
-      const v2f qf = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wf, 1.0f, pb);
-      const float t0 = fmaf(2.0f, qc[0], -qf[0]) * fmaf(4.0f, r0, -fmaf(2.0f, qc[0], qf[0]));
-      const float t1 = fmaf(2.0f, qc[1], -qf[1]) * fmaf(4.0f, r1, -fmaf(2.0f, qc[1], qf[1]));
-      delta += (int)(t0 * 4096.0f) + (int)(t1 * 4096.0f);
-    });
-    cc[j] = wc;
-    cf[j] = wf;
-  }
-  int e = (e_floor != e_ceil && delta < 0) ? e_floor : e_ceil;
+    for (int j = 0; j < 4; ++j) {
+      unsigned wc = 0u, wf = 0u;
+      static_for<4>([&](auto P_) {
+        constexpr int pb = decltype(P_)::value;
+        const unsigned word = raw[4 * j + pb];
+        const float v0 = __builtin_bit_cast(float, word << 16), v1 = __builtin_bit_cast(float, word & 0xffff0000u);
+        float r0, r1;
+        if constexpr (decltype(TWO_STEP_)::value) {
+          r0 = 6.0f * ldexpf(v0, -e_ceil);
+          r1 = 6.0f * ldexpf(v1, -e_ceil);
+        } else {
+          r0 = v0 * sc;
+          r1 = v1 * sc;
+        }
+        wc = cvt_pk_fp4<pb>(pb == 0 ? 0u : wc, r0, r1, 1.0f);
+        wf = cvt_pk_fp4<pb>(pb == 0 ? 0u : wf, r0, r1, 0.5f);
+        const v2f qc = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wc, 1.0f, pb);
+        const v2f qf = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wf, 1.0f, pb);
+        const float a0 = fmaf(2.0f, qc[0], -qf[0]), a1 = fmaf(2.0f, qc[1], -qf[1]);
+        s_ar = fmaf(a1, r1, fmaf(a0, r0, s_ar));
+        s_ab = fmaf(a1, fmaf(2.0f, qc[1], qf[1]), fmaf(a0, fmaf(2.0f, qc[0], qf[0]), s_ab));
+      });
+      cc[j] = wc;
+      cf[j] = wf;
+    }
+  };
+  if (e_ceil >= -125) convert(std::false_type{});
+  else convert(std::true_type{});
+  int e = (e_floor != e_ceil && 4.0f * s_ar < s_ab) ? e_floor : e_ceil;
   e = e < -127 ? -127 : (e > 127 ? 127 : e);
   if (e == e_ceil) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) codes[j] = cc[j] | sign[j];
+    for (int j = 0; j < 4; ++j) codes[j] = cc[j];
   } else if (e == e_floor) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) codes[j] = cf[j] | sign[j];
+    for (int j = 0; j < 4; ++j) codes[j] = cf[j];
   } else {  // amplitude clamped to the E8M0 range
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      unsigned w = 0u;
-      static_for<4>([&](auto P_) {
-        constexpr int pb = decltype(P_)::value;
-        const int k = 8 * j + 2 * pb;
-        w = cvt_pk_fp4<pb>(pb == 0 ? 0u : w, 6.0f * ldexpf(mag[k], -e), 6.0f * ldexpf(mag[k + 1], -e), 1.0f);
-      });
-      codes[j] = w | sign[j];
-    }
+    encode(e, codes);
   }
   return (unsigned)(e + 127);
 }
