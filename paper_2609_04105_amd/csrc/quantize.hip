@@ -292,6 +292,55 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_kernel(const uin
   *reinterpret_cast<v4i*>(codes + ((col0 + 1) * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
 }
 
+// bf16, blocks along rows with transposed output (V), staged: a workgroup takes
+// 64 columns x 256 rows (32 column pairs x 8 blocks; a thread quantizes one block
+// of two adjacent columns as above), parks its codes and scale bytes in LDS, and
+// writes each column's 8 blocks of codes as one contiguous 128-byte run.  The
+// loads stay 128-byte row segments.  cols % 64 == 0; blocks past the last are
+// skipped (their threads still meet the barrier).
+__global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_staged_kernel(
+    const uint16_t* __restrict__ src, int64_t batch, int64_t rows, int64_t cols, uint8_t* __restrict__ codes,
+    uint8_t* __restrict__ scales, int64_t n_anchor, int64_t anchor_stride) {
+  __shared__ uint4 code_lds[64][8];
+  __shared__ uint8_t scale_lds[64][8];
+  const int64_t nblk = rows / 32, ngrp = (nblk + 7) / 8, ncg = cols / 64;
+  const int64_t grp = blockIdx.x % ngrp, cg = (blockIdx.x / ngrp) % ncg, b = blockIdx.x / (ngrp * ncg);
+  const int tid = threadIdx.x, cp = tid % 32, lb = tid / 32;
+  const int64_t blk = grp * 8 + lb;
+  if (blk < nblk) {
+    const uint16_t* base = src + b * rows * cols + cg * 64 + 2 * cp;
+    unsigned pair[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+      pair[j] = *reinterpret_cast<const unsigned*>(base + anchor_source_row(blk * 32 + j, n_anchor, anchor_stride) * cols);
+    unsigned raw0[16], raw1[16];  // column 2 cp and 2 cp + 1, rows in order
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      raw0[i] = (pair[2 * i] & 0xffffu) | (pair[2 * i + 1] << 16);
+      raw1[i] = (pair[2 * i] >> 16) | (pair[2 * i + 1] & 0xffff0000u);
+    }
+    unsigned w[4];
+    scale_lds[2 * cp][lb] = (uint8_t)mxfp4_block_bf16(raw0, w);
+    code_lds[2 * cp][lb] = uint4{w[0], w[1], w[2], w[3]};
+    scale_lds[2 * cp + 1][lb] = (uint8_t)mxfp4_block_bf16(raw1, w);
+    code_lds[2 * cp + 1][lb] = uint4{w[0], w[1], w[2], w[3]};
+  }
+  __syncthreads();
+  // thread t writes blocks 2 (t % 4) and 2 (t % 4) + 1 of column t / 4
+  const int c = tid / 4, part = tid % 4;
+  const int64_t col = b * cols + cg * 64 + c;
+  uint8_t* cdst = codes + (col * nblk + grp * 8) * 16;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int l = 2 * part + k;
+    if (grp * 8 + l < nblk) *reinterpret_cast<uint4*>(cdst + l * 16) = code_lds[c][l];
+  }
+  if (tid < 64) {
+    const int64_t colx = b * cols + cg * 64 + tid;
+    for (int l = 0; l < 8 && grp * 8 + l < nblk; ++l) scales[colx * nblk + grp * 8 + l] = scale_lds[tid][l];
+  }
+}
+
 // MXFP8 (E4M3 payload + E8M0 per 32 values): the amplitude is the smallest
 // power of two 2^e with amax / 2^e <= 448, so no payload saturates; payloads
 // are v / 2^e (exact) rounded to nearest even by the hardware converter, which
@@ -394,6 +443,12 @@ hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, 
   if (src_dtype == 1 && axis == 1) {
     hipLaunchKernelGGL(quantize_mxfp4_bf16_rows_kernel, grid, block, 0, stream, (const uint16_t*)src, batch, rows, cols,
                        codes, scales, n_anchor, stride);
+    return hipGetLastError();
+  }
+  if (src_dtype == 1 && axis == 0 && cols % 64 == 0) {
+    const int64_t groups = batch * (cols / 64) * ((nblk + 7) / 8);
+    hipLaunchKernelGGL(quantize_mxfp4_bf16_cols_staged_kernel, dim3((unsigned)groups), block, 0, stream,
+                       (const uint16_t*)src, batch, rows, cols, codes, scales, n_anchor, stride);
     return hipGetLastError();
   }
   if (src_dtype == 1 && axis == 0 && cols % 2 == 0) {

@@ -94,15 +94,19 @@ def _adversarial_bf16_blocks():
     return torch.stack(blocks).to(torch.bfloat16)                            # [32 blocks, 32]
 
 
-@pytest.mark.parametrize("axis", [-1, -2])
-def test_adversarial_blocks_bf16(fa, axis):
+@pytest.mark.parametrize("axis,cols", [(-1, 32), (-2, 8), (-2, 64)])
+def test_adversarial_blocks_bf16(fa, axis, cols):
     """The bf16 kernels: one block per row (axis -1), or four blocks of 32 rows
-    down each of 8 columns (axis -2), so both layouts of the fast path run."""
+    down each column (axis -2): 8 columns take the per-thread kernel, 64 columns
+    the kernel that stages its codes in LDS (the 32 blocks repeated with
+    alternating signs)."""
     x = _adversarial_bf16_blocks()
     if axis == -1:
         x = x.reshape(1, 32, 32)
     else:                                      # block (g, c) = rows 32 g .. 32 g + 31 of column c
-        x = x.reshape(4, 8, 32).permute(0, 2, 1).reshape(1, 128, 8).contiguous()
+        reps = 4 * cols // 32
+        x = torch.cat([x * (-1) ** k for k in range(reps)])
+        x = x.reshape(4, cols, 32).permute(0, 2, 1).reshape(1, 128, cols).contiguous()
     _check(fa, x, axis)
 
 
