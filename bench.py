@@ -14,8 +14,8 @@ inputs (windows interleaved with the FP4 ones, the paper's speedup
 t_BF16 / t_FP4), the roofline of the forward kernel against the dense MXFP4
 matrix peak (and, beside it, the shader clock the kernel ran at and the rate
 a stream of FP4 matrix products alone sustains on the workload's K and Q
-codes), both kernels on the six shapes of the paper's primary forward
-comparison next to the paper's printed rates, and the CPU oracle timed on a
+codes), both kernels on the shapes the paper reports (D128 and D64) next to
+the paper's printed rates, and the CPU oracle timed on a
 bounded sample of rows.  The
 defaults follow the paper's timing protocol (Sec. "Operator benchmark suites"): 240
 warmup steps (over 300 ms), 2200 timed steps (about 3 s), and ten interleaved
@@ -184,20 +184,24 @@ def sustained_mfma_tflops(torch, fa, a_codes, b_codes, blocks=1024, iters=100000
     return flop / (ms * 1e-3) / 1e12
 
 
-# The paper's retained route (NV/MX `fast`) on the six shapes of its primary forward
-# comparison (B1, D128; Table primary-results): TFLOP/s as printed there for its
-# GB200 and B300 systems (None: not run).  Context for the same shapes here, not a
-# target: other hardware, and NVFP4 Q/K where this path uses MXFP4.
-PAPER_SHAPES = {(24, 4096): (2237, 2369), (64, 4096): (2711, 2901), (64, 6144): (2731, 2958),
-                (64, 8192): (2900, 3116), (64, 9472): (None, 3159), (24, 32768): (2998, 2945)}
+# The paper's retained route (NV/MX) on the shapes it reports, B1: TFLOP/s as
+# printed for its GB200 and B300 systems (None: not run) -- D128 from its primary
+# forward comparison (Table primary-results), D64 from its B300 D64 diagnostics
+# (Table b300-d64-diagnostic).  Context for the same shapes here, not a target:
+# other hardware, and NVFP4 Q/K where this path uses MXFP4.
+PAPER_SHAPES = {(128, 24, 4096): (2237, 2369), (128, 64, 4096): (2711, 2901), (128, 64, 6144): (2731, 2958),
+                (128, 64, 8192): (2900, 3116), (128, 64, 9472): (None, 3159), (128, 24, 32768): (2998, 2945),
+                (64, 12, 4096): (None, 775), (64, 24, 4096): (None, 1105), (64, 24, 32768): (None, 1434),
+                (64, 32, 2048): (None, 862), (64, 32, 32768): (None, 1438), (64, 64, 1024): (None, 672),
+                (64, 64, 4096): (None, 1323), (64, 64, 32768): (None, 1439)}
 
 
-def paper_shape_sweep(torch, fa, d=128, seed=20):
-    """The MXFP4 forward and the BF16 kernel on the paper's primary shapes: N(0, 1)
+def paper_shape_sweep(torch, fa, seed=20):
+    """The MXFP4 forward and the BF16 kernel on the paper's reported shapes: N(0, 1)
     bf16 inputs drawn on the GPU, windows of the two kernels interleaved."""
     res = []
     g = torch.Generator(device="cuda").manual_seed(seed)
-    for (H, S), (gb200, b300) in PAPER_SHAPES.items():
+    for (d, H, S), (gb200, b300) in PAPER_SHAPES.items():
         q, k, v = (torch.randn((1, H, S, d), device="cuda", generator=g, dtype=torch.float32).to(torch.bfloat16)
                    for _ in range(3))
         ops = fa.quantize_qkv(q, k, v)
@@ -213,7 +217,7 @@ def paper_shape_sweep(torch, fa, d=128, seed=20):
         res.append({"shape": f"B1/S{S}/H{H}/D{d}", "tflops": round(flop / (med["fp4"] * 1e-3) / 1e12, 1),
                     "bf16_tflops": round(flop / (med["bf16"] * 1e-3) / 1e12, 1),
                     "speedup_vs_bf16": round(med["bf16"] / med["fp4"], 3),
-                    "paper_fast_tflops": {"gb200": gb200, "b300": b300}})
+                    "paper_nvmx_tflops": {"gb200": gb200, "b300": b300}})
         del q, k, v, ops, vt, out
     return res
 
@@ -266,7 +270,7 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
-    ap.add_argument("--no-paper-shapes", action="store_true", help="skip the paper's primary shapes")
+    ap.add_argument("--no-paper-shapes", action="store_true", help="skip the paper's reported shapes")
     ap.add_argument("--traffic-run", action="store_true",
                     help="for rocprofv3 --pmc passes: one 256 MiB device copy (counter calibration), "
                          "then one forward launch; prints no JSON")
