@@ -347,6 +347,43 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_staged_kernel(
 // keeps E4M3 subnormals.  Zero block: u = 0; non-finite block: u = 255, codes 0.
 // Codes are stored one byte per value, in the same orientation as the MXFP4
 // quantizer (axis 0: transposed).
+// One MXFP8 block: returns the E8M0 byte; w[i] holds the E4M3 payloads of values
+// 4 i .. 4 i + 3.
+__device__ __forceinline__ unsigned mxfp8_block(const float (&v)[32], unsigned (&w)[8]) {
+  float amax = 0.0f;
+  bool finite = true;
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    finite = finite && __builtin_isfinite(v[j]);
+    amax = fmaxf(amax, fabsf(v[j]));
+  }
+  unsigned ubyte;
+  int e = 0;
+  if (!finite) {
+    ubyte = 255;
+  } else if (amax == 0.0f) {
+    ubyte = 0;
+  } else {
+    int x;
+    frexpf(amax, &x);          // amax = m 2^x, m in [0.5, 1)
+    e = x - 9;                 // amax / 2^e in [256, 512)
+    if (ldexpf(amax, -e) > 448.0f) ++e;
+    e = e < -127 ? -127 : (e > 127 ? 127 : e);
+    ubyte = (unsigned)(e + 127);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if (finite) {
+      const float a0 = ldexpf(v[4 * i], -e), a1 = ldexpf(v[4 * i + 1], -e);
+      const float a2 = ldexpf(v[4 * i + 2], -e), a3 = ldexpf(v[4 * i + 3], -e);
+      w[i] = cvt_pk_fp8<true>(cvt_pk_fp8<false>(0u, a0, a1), a2, a3);
+    } else {
+      w[i] = 0u;
+    }
+  }
+  return ubyte;
+}
+
 template <typename T, int AXIS>
 __global__ __launch_bounds__(256) void quantize_mxfp8_kernel(const T* __restrict__ src, int64_t batch, int64_t rows,
                                                              int64_t cols, uint8_t* __restrict__ codes,
@@ -376,42 +413,63 @@ __global__ __launch_bounds__(256) void quantize_mxfp8_kernel(const T* __restrict
 #pragma unroll
     for (int j = 0; j < 32; ++j) v[j] = load_as_float<T>(p + (int64_t)j * cols);
   }
-  float amax = 0.0f;
-  bool finite = true;
-#pragma unroll
-  for (int j = 0; j < 32; ++j) {
-    finite = finite && __builtin_isfinite(v[j]);
-    amax = fmaxf(amax, fabsf(v[j]));
-  }
-  unsigned ubyte;
-  int e = 0;
-  if (!finite) {
-    ubyte = 255;
-  } else if (amax == 0.0f) {
-    ubyte = 0;
-  } else {
-    int x;
-    frexpf(amax, &x);          // amax = m 2^x, m in [0.5, 1)
-    e = x - 9;                 // amax / 2^e in [256, 512)
-    if (ldexpf(amax, -e) > 448.0f) ++e;
-    e = e < -127 ? -127 : (e > 127 ? 127 : e);
-    ubyte = (unsigned)(e + 127);
-  }
   unsigned w[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    if (finite) {
-      const float a0 = ldexpf(v[4 * i], -e), a1 = ldexpf(v[4 * i + 1], -e);
-      const float a2 = ldexpf(v[4 * i + 2], -e), a3 = ldexpf(v[4 * i + 3], -e);
-      w[i] = cvt_pk_fp8<true>(cvt_pk_fp8<false>(0u, a0, a1), a2, a3);
-    } else {
-      w[i] = 0u;
-    }
-  }
+  const unsigned ubyte = mxfp8_block(v, w);
   uint8_t* cdst = codes + (b * outer + o) * (nblk * 32) + blk * 32;
   *reinterpret_cast<v4i*>(cdst) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
   *reinterpret_cast<v4i*>(cdst + 16) = v4i{(int)w[4], (int)w[5], (int)w[6], (int)w[7]};
   scales[(b * outer + o) * nblk + blk] = (uint8_t)ubyte;
+}
+
+// MXFP8 of bf16 blocks along rows with transposed output (V of the FP8 P/V
+// route), staged like the MXFP4 V^T kernel: a workgroup takes 64 columns x 256
+// rows (32 column pairs x 8 blocks, 4-byte row loads), parks its payloads and
+// scale bytes in LDS and writes each column's 8 blocks as one 256-byte run.
+// cols % 64 == 0; blocks past the last are skipped (their threads still meet
+// the barrier).
+__global__ __launch_bounds__(256) void quantize_mxfp8_bf16_cols_staged_kernel(
+    const uint16_t* __restrict__ src, int64_t batch, int64_t rows, int64_t cols, uint8_t* __restrict__ codes,
+    uint8_t* __restrict__ scales) {
+  __shared__ uint4 code_lds[64][8][2];
+  __shared__ uint8_t scale_lds[64][8];
+  const int64_t nblk = rows / 32, ngrp = (nblk + 7) / 8, ncg = cols / 64;
+  const int64_t grp = blockIdx.x % ngrp, cg = (blockIdx.x / ngrp) % ncg, b = blockIdx.x / (ngrp * ncg);
+  const int tid = threadIdx.x, cp = tid % 32, lb = tid / 32;
+  const int64_t blk = grp * 8 + lb;
+  if (blk < nblk) {
+    const uint16_t* base = src + (b * rows + blk * 32) * cols + cg * 64 + 2 * cp;
+    float v0[32], v1[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const unsigned pr = *reinterpret_cast<const unsigned*>(base + (int64_t)j * cols);
+      v0[j] = __builtin_bit_cast(float, pr << 16);
+      v1[j] = __builtin_bit_cast(float, pr & 0xffff0000u);
+    }
+    unsigned w[8];
+    scale_lds[2 * cp][lb] = (uint8_t)mxfp8_block(v0, w);
+    code_lds[2 * cp][lb][0] = uint4{w[0], w[1], w[2], w[3]};
+    code_lds[2 * cp][lb][1] = uint4{w[4], w[5], w[6], w[7]};
+    scale_lds[2 * cp + 1][lb] = (uint8_t)mxfp8_block(v1, w);
+    code_lds[2 * cp + 1][lb][0] = uint4{w[0], w[1], w[2], w[3]};
+    code_lds[2 * cp + 1][lb][1] = uint4{w[4], w[5], w[6], w[7]};
+  }
+  __syncthreads();
+  // thread t writes blocks 2 (t % 4) and 2 (t % 4) + 1 of column t / 4
+  const int c = tid / 4, part = tid % 4;
+  const int64_t col = b * cols + cg * 64 + c;
+  uint8_t* cdst = codes + (col * nblk + grp * 8) * 32;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int l = 2 * part + k;
+    if (grp * 8 + l < nblk) {
+      *reinterpret_cast<uint4*>(cdst + l * 32) = code_lds[c][l][0];
+      *reinterpret_cast<uint4*>(cdst + l * 32 + 16) = code_lds[c][l][1];
+    }
+  }
+  if (tid < 64) {
+    const int64_t colx = b * cols + cg * 64 + tid;
+    for (int l = 0; l < 8 && grp * 8 + l < nblk; ++l) scales[colx * nblk + grp * 8 + l] = scale_lds[tid][l];
+  }
 }
 
 // dst[b, c, r] = src[b, r, c] for bf16, through a 64 x 64 LDS tile.
@@ -481,6 +539,12 @@ hipError_t launch_quantize_mxfp8(const void* src, int src_dtype, int64_t batch, 
   const int64_t outer = axis == 1 ? rows : cols;
   const int64_t total = batch * outer * nblk;
   const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  if (src_dtype == 1 && axis == 0 && cols % 64 == 0) {
+    const int64_t groups = batch * (cols / 64) * ((nblk + 7) / 8);
+    hipLaunchKernelGGL(quantize_mxfp8_bf16_cols_staged_kernel, dim3((unsigned)groups), block, 0, stream,
+                       (const uint16_t*)src, batch, rows, cols, codes, scales);
+    return hipGetLastError();
+  }
   if (src_dtype == 0) {
     if (axis == 1)
       hipLaunchKernelGGL((quantize_mxfp8_kernel<float, 1>), grid, block, 0, stream, (const float*)src, batch, rows,

@@ -192,6 +192,35 @@ def test_mxfp8_adversarial_blocks(fa, axis):
     _check8(fa, x, axis)
 
 
+@pytest.mark.parametrize("shape", [(3, 96, 192), (2, 256, 64)])
+def test_mxfp8_staged_bf16(fa, shape):
+    """bf16 V^T with whole 64-column groups takes the staged kernel: a ragged
+    last group of blocks (96 rows) and full ones, values over 40 binades."""
+    g = torch.Generator().manual_seed(shape[1] + shape[2])
+    x = (torch.randn(*shape, generator=g) * torch.exp2(torch.randint(-20, 20, shape, generator=g))).to(torch.bfloat16)
+    _check8(fa, x, -2)
+
+
+def test_mxfp8_adversarial_blocks_bf16_staged(fa):
+    """The adversarial blocks rounded to bf16, one per column of a 64-column
+    matrix, through the staged V^T kernel."""
+    from oracle import fp8pv
+    grid = torch.tensor(fp8pv.E4M3, dtype=torch.float64)
+    mids = ((grid[1:] + grid[:-1]) / 2)[:32]
+    blocks = torch.stack([
+        torch.cat([torch.tensor([448.0]), mids[:31]]),
+        torch.cat([torch.tensor([448.0]), grid[1:32] * 0.75]),
+        torch.cat([torch.tensor([480.0]), -mids[:31]]),                      # above 448 in bf16
+        torch.zeros(32),
+        torch.cat([torch.tensor([-0.0, 1.0]), torch.zeros(30)]),
+        torch.cat([torch.tensor([float("nan")]), torch.ones(31)]),
+        torch.cat([torch.tensor([float("inf")]), torch.ones(31)]),
+        torch.linspace(-1e-3, 1e-3, 32),
+    ]).to(torch.float32)
+    x = blocks[torch.arange(64) % 8].transpose(0, 1).reshape(1, 32, 64).to(torch.bfloat16).contiguous()
+    _check8(fa, x, -2)
+
+
 def test_mxfp8_workload_v(fa):
     from oracle import fp8pv
     q, k, v = workloads.generate("outlier_b2h16_n4096_d128")
