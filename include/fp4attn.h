@@ -68,7 +68,8 @@ typedef enum {
  *
  * Errors: INVALID_ARG if a pointer is null or misaligned, batch < 1, rows < 1,
  * cols < 1, the blocked extent (cols for axis 1, rows for axis 0) is not a
- * multiple of 32, axis is not 0 or 1, or src_dtype is not a fp4attn_dtype.
+ * multiple of 32, axis is not 0 or 1, src_dtype is not a fp4attn_dtype, or
+ * the tensor holds more than 2^40 blocks of 32.
  * The quantizer is not part of the timed forward (the paper times the kernel
  * on prequantized operands).
  */
@@ -133,7 +134,8 @@ fp4attn_status fp4attn_quantize_mxfp4_anchored(const void* src, int src_dtype, i
  *
  * Errors: INVALID_ARG for null/misaligned pointers, B < 1, H < 1, N < 128 or
  * N % 128 != 0, softmax_scale not finite or <= 0, affine_a not finite or <= 0,
- * affine_b not finite, bad out_dtype, or B*H*N beyond 2^31.  UNSUPPORTED for
+ * affine_b not finite, bad out_dtype, B*H*N beyond 2^31 - 1 or B*H beyond
+ * 16776960 (65535 * 256).  UNSUPPORTED for
  * d not in {64, 128} or N above 4194304 (2^22) keys.  Non-finite operands (E8M0 byte 255) give unspecified but
  * non-faulting results for the rows they touch.
  */
@@ -253,7 +255,8 @@ fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* vt
  * Layout helper for the BF16 baseline: dst[b, c, r] = src[b, r, c] for
  * `batch` bf16 [rows, cols] matrices.  Not part of the timed forward, like the
  * quantizer.  Errors: INVALID_ARG for null/misaligned pointers, batch/rows/cols
- * < 1, rows or cols not a multiple of 8.
+ * < 1, rows or cols not a multiple of 8, batch above 65535 or rows above
+ * 65535 * 64.
  */
 fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols,
                                       void* dst, void* stream);

@@ -49,8 +49,10 @@ fp4attn_status check_attention_shape(int64_t B, int64_t H, int64_t N, int64_t d,
     return fail(FP4ATTN_ERR_INVALID_ARG, "softmax_scale must be finite and positive");
   if (out_dtype != FP4ATTN_F32 && out_dtype != FP4ATTN_BF16)
     return fail(FP4ATTN_ERR_INVALID_ARG, "out_dtype %d is not FP4ATTN_F32 or FP4ATTN_BF16", out_dtype);
-  if (B * H * N > (int64_t(1) << 31) - 1 || B * H > 65535 * 256)
-    return fail(FP4ATTN_ERR_INVALID_ARG, "B*H*N=%lld exceeds 2^31", (long long)(B * H * N));
+  // B and H first, so that no product below can overflow 64 bits
+  if (B > 65535 * 256 || H > 65535 * 256 || B * H > 65535 * 256 || B * H > ((int64_t(1) << 31) - 1) / N)
+    return fail(FP4ATTN_ERR_INVALID_ARG, "B=%lld H=%lld N=%lld: B*H*N must stay below 2^31 and B*H below 2^24",
+                (long long)B, (long long)H, (long long)N);
   if (d != 64 && d != 128) return fail(FP4ATTN_ERR_UNSUPPORTED, "head dimension d=%lld is not 64 or 128", (long long)d);
   // one head's operands (FP8 V^T: d N bytes) and every in-head byte offset stay below 2^31
   if (N > kMaxN) return fail(FP4ATTN_ERR_UNSUPPORTED, "N=%lld exceeds %lld keys", (long long)N, (long long)kMaxN);
@@ -169,7 +171,9 @@ fp4attn_status quantize_common(const void* src, int src_dtype, int64_t batch, in
   const int64_t blocked = axis == 1 ? cols : rows, other = axis == 1 ? rows : cols;
   if (blocked % 32 != 0)
     return fail(FP4ATTN_ERR_INVALID_ARG, "the blocked extent (%lld) must be a multiple of 32", (long long)blocked);
-  if (batch * other * (blocked / 32) > (int64_t(1) << 40))
+  // divisions instead of products, so that no check can overflow 64 bits
+  const int64_t kMaxBlocks = int64_t(1) << 40;
+  if (other > kMaxBlocks / batch || blocked / 32 > kMaxBlocks / (batch * other))
     return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large");
   if ((batch * other * (blocked / 32) + 255) / 256 > 0x7fffffff)
     return fail(FP4ATTN_ERR_INVALID_ARG, "tensor too large for one launch");

@@ -63,6 +63,9 @@ def test_forward_validation(lib):
     assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, FAKE[6], 3, None) == 1
     assert f(*FAKE[:6], 1, 1, 128, 64, 0.125, 1.5, 1.2, ctypes.c_void_p(4100), 0, None) == 1
     assert f(*FAKE[:6], 1 << 20, 1 << 10, 1 << 12, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1
+    # sizes whose products would overflow 64 bits are refused, not wrapped
+    for B, H, N in ((1 << 62, 1 << 62, 128), (1, 1, 1 << 62), (1 << 40, 1, 1 << 40), (4097, 4097, 128)):
+        assert f(*FAKE[:6], B, H, N, 64, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 1, (B, H, N)
     # one head's operands must stay addressable with 32-bit offsets: N up to 2^22 keys
     assert f(*FAKE[:6], 1, 1, (1 << 22) + 128, 128, 0.125, 1.5, 1.2, FAKE[6], 0, None) == 2
 
@@ -74,6 +77,9 @@ def test_quantize_and_bf16_validation(lib):
     assert q(FAKE[0], 2, 1, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # dtype
     assert q(FAKE[0], 0, 1, 4, 64, 2, FAKE[1], FAKE[2], None) == 1     # axis
     assert q(FAKE[0], 0, 0, 4, 64, 1, FAKE[1], FAKE[2], None) == 1     # batch
+    for batch, rows, cols in ((1 << 62, 1 << 62, 64), (1, 1 << 62, 1 << 62), (1 << 20, 1 << 20, 1 << 12)):
+        assert q(FAKE[0], 0, batch, rows, cols, 1, FAKE[1], FAKE[2], None) == 1, (batch, rows, cols)
+        assert q(FAKE[0], 0, batch, cols, rows, 0, FAKE[1], FAKE[2], None) == 1, (batch, rows, cols)
     q8 = lib.fp4attn_quantize_mxfp8
     assert q8(FAKE[0], 0, 1, 4, 48, 1, FAKE[1], FAKE[2], None) == 1    # cols not /32
     assert q8(None, 0, 1, 4, 64, 1, FAKE[1], FAKE[2], None) == 1
