@@ -240,6 +240,58 @@ def test_extreme_logits_stay_finite(fa):
     assert torch.isfinite(out).all()
 
 
+@pytest.mark.parametrize("case", ["q_zero", "v_zero", "v_pow2"])
+def test_degenerate_inputs(fa, case):
+    """Degenerate inputs of the method, on a launch of several tiles.  Q = 0: every
+    score is 0, so every block has E_B = 0 and one code everywhere, and O is the
+    mean of the represented V rows.  V = 0: O = 0 exactly.  V = 2^-3 everywhere:
+    every V block is represented exactly, so O = 2^-3 up to fp32 summation."""
+    g = torch.Generator().manual_seed(12)
+    B, H, N, d = 1, 2, 640, 128
+    q, k, v = (torch.randn(B, H, N, d, generator=g) for _ in range(3))
+    if case == "q_zero":
+        q.zero_()
+    elif case == "v_zero":
+        v.zero_()
+    else:
+        v.fill_(0.125)
+    q, k, v = (t.to(torch.bfloat16) for t in (q, k, v))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    rows = np.arange(B * H * N)
+    print(f"[degenerate {case}] B{B} H{H} N{N} d{d}", flush=True)
+    ops = gpu_operands(q.cuda(), k.cuda(), v.cuda())
+    dump = fa.debug_directp_mxfp4(*ops, torch.from_numpy(rows).cuda())
+    out = fa.forward_mxfp4(*ops)
+    torch.cuda.synchronize()
+    assert torch.equal(out, dump["out"])
+    ref = oracle_rows(*host64, rows, 1.0 / np.sqrt(d))
+    mismatch = check_directp_dump(dump, ref, case)
+    got = out.reshape(-1, d).cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all()
+    if case == "q_zero":
+        assert np.all(ref["E"] == 0) and np.all(ref["codes"] == ref["codes"][0, 0])
+        vhat = np.stack([fa_oracle_vhat(host64[2][0, h]) for h in range(H)])      # [H, N, d]
+        mean = vhat.mean(axis=1)                                                 # [H, d]
+        np.testing.assert_allclose(got.reshape(H, N, d), np.broadcast_to(mean[:, None], (H, N, d)),
+                                   rtol=1e-5, atol=2e-6)
+    elif case == "v_zero":
+        assert np.all(got == 0.0)
+    else:
+        np.testing.assert_allclose(got, 0.125, rtol=1e-5, atol=0)
+    if case != "v_zero":
+        rel, cos = rel_l2_cos(got, ref["O"])
+        assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{case}: rel {rel} cos {cos}"
+    print(f"[degenerate {case}] code mismatch {mismatch:.2e}", flush=True)
+
+
+def fa_oracle_vhat(v):
+    """Represented V̂ [N, d] of one head: the oracle's MXFP4 quantization along
+    the sequence, decoded."""
+    from oracle import mxfp4
+    codes, scales = mxfp4.quantize(v, axis=-2)          # stored transposed: [d, N]
+    return mxfp4.dequantize(codes, scales).T
+
+
 def test_deterministic_and_fully_overwritten(fa):
     host64, dev = load_workload("small_b1h8_n1024_d64")
     ops = gpu_operands(*dev)
