@@ -90,6 +90,17 @@ def test_wide_launch_two_tiles(fa):
     _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, B * H * N, 5), "wide two tiles")
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_half_round_tail_launch(fa, d):
+    """B1 H24 N4096: 384 eight-wave workgroups would leave the second round half
+    empty, so the launch takes four-wave workgroups; every 23rd row checked."""
+    g = torch.Generator().manual_seed(9)
+    B, H, N = 1, 24, 4096
+    q, k, v = (torch.randn(B, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, B * H * N, 23), f"tail d{d}")
+
+
 @pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "student_t_b1h32_n8192_d128",
                                   "long_b1h32_n16384_d128"])
 def test_full_size_sampled_rows(fa, name):
@@ -334,7 +345,9 @@ def test_error_paths_do_not_launch(fa):
 
 
 @pytest.mark.parametrize("n_dump", [0, 1])
-@pytest.mark.parametrize("B,H,N,d,wgs", [(1, 2, 384, 128, 6), (1, 128, 512, 128, 256)])
+# (1, 24, 4096, 128): 384 eight-wave workgroups would leave a half-empty second
+# round, so the launch takes 768 four-wave ones
+@pytest.mark.parametrize("B,H,N,d,wgs", [(1, 2, 384, 128, 6), (1, 128, 512, 128, 256), (1, 24, 4096, 128, 768)])
 def test_workgroup_clock_record(fa, B, H, N, d, wgs, n_dump):
     """The test entry point's per-workgroup clock record, with and without rows to
     dump: exactly the launch's workgroups write it, with a plausible shader clock,
