@@ -99,12 +99,15 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   // Eight waves (256 rows) per workgroup when that still fills the 256 CUs.
   // (the FP8 P/V route too: its d = 128 form spills a few registers with eight
   // waves, but four waves leave one per SIMD, since its LDS ring takes 108 KiB)
-  // One exception: when the eight-wave grid takes a second round that is at most
-  // half full (257 to 384 workgroups), four-wave workgroups, two per CU, finish
-  // the tail sooner (5 % at B1 H24 N4096 d128, while a full last round favours
-  // eight waves by 4-7 %); the FP8 route and the causal forward keep eight waves.
+  // One exception: when the eight-wave grid takes two to five rounds and its last
+  // round is at most half full, four-wave workgroups, two per CU, finish the tail
+  // sooner (B1 N4096 d128: +9 % at H24, +10 % at H36, +4 % at H40, +3 % at H72;
+  // -2 % with ten rounds at H64 N9472, and a full last round favours eight waves
+  // by 4-7 %).  The FP8 route and the causal forward keep eight waves.
   const int64_t wide_wgs = a.N % 256 == 0 ? (int64_t)(a.N / 256) * bh : 0;
-  const bool wide = wide_wgs >= 256 && !(wide_wgs > 256 && wide_wgs <= 384 && !a.pv_fp8 && !a.causal);
+  const int64_t last_round = wide_wgs % 256;
+  const bool tail = wide_wgs > 256 && wide_wgs <= 5 * 256 && last_round != 0 && last_round <= 128;
+  const bool wide = wide_wgs >= 256 && !(tail && !a.pv_fp8 && !a.causal);
   const int BM = wide ? 256 : 128;
   kp.n_qtiles = a.N / BM;
   kp.total = kp.n_qtiles * bh;

@@ -347,7 +347,10 @@ def test_error_paths_do_not_launch(fa):
 @pytest.mark.parametrize("n_dump", [0, 1])
 # (1, 24, 4096, 128): 384 eight-wave workgroups would leave a half-empty second
 # round, so the launch takes 768 four-wave ones
-@pytest.mark.parametrize("B,H,N,d,wgs", [(1, 2, 384, 128, 6), (1, 128, 512, 128, 256), (1, 24, 4096, 128, 768)])
+# (1, 36, 4096, 64): 576 eight-wave workgroups, a third round a quarter full: 1152
+# four-wave ones; (1, 32, 4096, 128): 512, two full rounds: eight waves
+@pytest.mark.parametrize("B,H,N,d,wgs", [(1, 2, 384, 128, 6), (1, 128, 512, 128, 256), (1, 24, 4096, 128, 768),
+                                         (1, 36, 4096, 64, 1152), (1, 32, 4096, 128, 512)])
 def test_workgroup_clock_record(fa, B, H, N, d, wgs, n_dump):
     """The test entry point's per-workgroup clock record, with and without rows to
     dump: exactly the launch's workgroups write it, with a plausible shader clock,
