@@ -57,3 +57,13 @@ def test_bf16_tiny(fa):
 def test_bf16_full_size_sampled(fa, name):
     host64, dev = load_workload(name)
     _check(fa, host64, dev, workloads.sampled_rows(name)[::4], name)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_bf16_tail_launch(fa, d):
+    """B1 H24 N4096: the four-wave tail launch (384 eight-wave workgroups would
+    leave a half-empty second round); every 97th row checked."""
+    g = torch.Generator().manual_seed(10)
+    q, k, v = (torch.randn(1, 24, 4096, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    _check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, 24 * 4096, 97), f"tail d{d}")
