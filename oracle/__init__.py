@@ -31,6 +31,8 @@ prange   the probability-format range diagnostic of Table p-range
          (NVFP4 with global factor G, and MXFP4 probabilities).
 
 Every function is pinned by ``tests/test_oracle_*.py`` against values the
-paper prints, closed forms, invariants or brute force; none is marked
-"parity unpinned".
+paper prints, closed forms, invariants or brute force.  ``exact.attention`` is
+pinned by a scalar-loop brute force and closed forms, and
+``exact.attention_online`` against it for tile widths that divide N, leave a
+ragged last tile or exceed N (``tests/test_oracle_exact.py``).
 """

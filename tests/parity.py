@@ -10,14 +10,17 @@ from oracle import directp, e2m1, mxfp4
 CODE_MISMATCH_MAX = 1e-4   # fraction of Direct-P codes allowed to differ (rounding ties)
 O_REL_L2_MAX = 2e-3        # output relative L2 error bound
 O_COS_MIN = 0.9999         # output cosine bound
+O_ROW_REL_L2_MAX = 2e-3    # the same relative L2 bound on every checked row on its own
 
 
 def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_codes=True, ex2_pairs=0,
-                causal=False):
+                causal=False, mode="affine32"):
     """Run the oracle on flattened query ``rows`` of fp64 arrays q, k, v [B, H, N, d].
 
     The oracle quantizes its own operands (oracle.mxfp4).  Returns a dict of
-    row-aligned arrays: O, E, M, D and (optionally) codes.
+    row-aligned arrays: O, E, M, D and (optionally) codes.  ``mode`` is the
+    oracle's code decision: ``affine32`` (the fp32 fused multiply-add) or
+    ``affine64`` (eq. affine-code-map written out in fp64).
     """
     B, H, N, d = q.shape
     rows = np.asarray(rows, dtype=np.int64)
@@ -33,10 +36,42 @@ def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_c
         qc, qs = mxfp4.quantize(q[b, h], axis=-1)
         kc, ks = mxfp4.quantize(k[b, h], axis=-1)
         vc, vs = mxfp4.quantize(v[b, h], axis=-2)
-        res = directp.forward_rows(qc, qs, kc, ks, vc, vs, local, softmax_scale,
-                                   affine_a, affine_b, want_codes=want_codes, ex2_pairs=ex2_pairs, causal=causal)
+        res = directp.forward_rows(qc, qs, kc, ks, vc, vs, local, softmax_scale, affine_a, affine_b, mode=mode,
+                                   want_codes=want_codes, ex2_pairs=ex2_pairs, causal=causal)
         for key in res:
             out[key][sel] = res[key]
+    return out
+
+
+def oracle_rows_two_maps(q, k, v, rows, softmax_scale, workers=8):
+    """Codes and block exponents of flattened query ``rows`` under both code
+    decisions of the oracle, from one quantization of each head: ``affine64``
+    (eq. affine-code-map written out in fp64, with its output O) and
+    ``affine32`` (the fp32 fused multiply-add).  Heads run on a thread pool."""
+    from concurrent.futures import ThreadPoolExecutor
+    B, H, N, d = q.shape
+    rows = np.asarray(rows, dtype=np.int64)
+    heads = rows // N
+    out = {"codes64": np.zeros((len(rows), N), dtype=np.uint8), "E64": np.zeros((len(rows), N // 32), np.int64),
+           "codes32": np.zeros((len(rows), N), dtype=np.uint8), "E32": np.zeros((len(rows), N // 32), np.int64),
+           "O64": np.zeros((len(rows), d))}
+
+    def one_head(bh):
+        b, h = divmod(int(bh), H)
+        sel = np.nonzero(heads == bh)[0]
+        local = rows[sel] % N
+        qc, qs = mxfp4.quantize(q[b, h][local], axis=-1)
+        kc, ks = mxfp4.quantize(k[b, h], axis=-1)
+        vc, vs = mxfp4.quantize(v[b, h], axis=-2)
+        res = directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(local)), softmax_scale, mode="affine64")
+        raw = directp.raw_scores(mxfp4.scaled_operand(qc, qs), mxfp4.scaled_operand(kc, ks))
+        E32, _, k32 = directp.block_exponents_and_codes(raw, softmax_scale, 1.5, 1.2, "affine32")
+        return sel, res, E32, k32
+
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        for sel, res, E32, k32 in ex.map(one_head, np.unique(heads)):
+            out["codes64"][sel], out["E64"][sel], out["O64"][sel] = res["codes"], res["E"], res["O"]
+            out["codes32"][sel], out["E32"][sel] = k32, E32
     return out
 
 
@@ -46,6 +81,31 @@ def rel_l2_cos(a, b):
     rel = np.linalg.norm(a - b) / np.linalg.norm(b)
     cos = a @ b / (np.linalg.norm(a) * np.linalg.norm(b))
     return float(rel), float(cos)
+
+
+def row_rel_l2(a, b):
+    """Per-row relative L2 error ||a_i - b_i|| / ||b_i|| of [R, d] arrays.  A row
+    whose reference is exactly zero counts as 0 if the row matches exactly, else inf."""
+    a = np.asarray(a, dtype=np.float64).reshape(len(b), -1)
+    b = np.asarray(b, dtype=np.float64).reshape(len(b), -1)
+    num = np.linalg.norm(a - b, axis=1)
+    den = np.linalg.norm(b, axis=1)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return np.where(den > 0, num / np.where(den > 0, den, 1.0), np.where(num == 0, 0.0, np.inf))
+
+
+def check_output(got, ref, label):
+    """The output gates: global relative L2 and cosine over all checked rows, and
+    the relative L2 of every row on its own (so that an error confined to a few
+    rows cannot hide in the global norm).  Returns (rel, cos, worst row rel)."""
+    rel, cos = rel_l2_cos(got, ref)
+    rows = row_rel_l2(got, ref)
+    worst = float(rows.max()) if rows.size else 0.0
+    print(f"[{label}] O rel-L2 {rel:.3e}  cos {cos:.10f}  worst row rel-L2 {worst:.3e} "
+          f"(row {int(rows.argmax()) if rows.size else -1} of {len(rows)})", flush=True)
+    assert rel <= O_REL_L2_MAX and cos >= O_COS_MIN, f"{label}: rel {rel} cos {cos}"
+    assert worst <= O_ROW_REL_L2_MAX, f"{label}: row {int(rows.argmax())} rel-L2 {worst:.3e}"
+    return rel, cos, worst
 
 
 def unpack_codes(packed):
