@@ -36,16 +36,18 @@ HBM_PEAK_GBS = 8000.0
 SPEC_CLOCK_GHZ = 2.4          # the clock the spec peaks assume
 EX2_SWEEP = (1, 2, 4, 16)
 GUARD_ML = (110, 16)
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_mxfp4_long_b1h32_n16384_d128_traffic.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_04105_amd", "csrc", f)
-                  for f in ("fwd_mxfp4.hpp", "fwd_mxfp4.hip", "gfx950.hpp", "launch.hpp")]
+COUNTER_FILE = os.path.join(ROOT, "profiles", "counters_routes.json")
+CSRC = os.path.join(ROOT, "paper_2609_04105_amd", "csrc")
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("fwd_mxfp4.hpp", "fwd_mxfp4.hip", "gfx950.hpp", "launch.hpp")]
+BF16_SOURCES = [os.path.join(CSRC, f) for f in ("fwd_bf16.hip", "gfx950.hpp", "launch.hpp")]
 
 
-def _source_sha():
-    """Hash of the forward kernel's sources with comments and blank lines removed,
-    so that the committed counters stay attached to the code they measured."""
+def _source_sha(paths=None):
+    """Hash of kernel sources with comments and blank lines removed, so that the
+    committed counters stay attached to the code they measured (default: the
+    MXFP4 forward's sources)."""
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
+    for path in (paths or KERNEL_SOURCES):
         with open(path) as f:
             for line in f:
                 code = line.split("//", 1)[0].rstrip()
@@ -54,71 +56,194 @@ def _source_sha():
     return h.hexdigest()
 
 
-def _traffic():
-    """HBM bytes per forward launch from committed rocprofv3 counters, if they
-    were taken on the current kernel source; else None."""
-    try:
-        with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if t.get("source_sha256") != _source_sha():
-        return None
-    return t.get("bytes_per_launch")
+# Routes whose counters are committed (one launch each, in this order, under
+# ``--profile-run``): (label, inputs, kernel family, route options).  Inputs are a
+# workload name or a paper shape "d64_b1h64_n32768" (N(0, 1) bf16 drawn on the GPU).
+PROFILE_ROUTES = [
+    ("online", "long_b1h32_n16384_d128", "fp4", {}),
+    ("ex2_4", "long_b1h32_n16384_d128", "fp4", {"ex2_pairs": 4}),
+    ("ex2_16", "long_b1h32_n16384_d128", "fp4", {"ex2_pairs": 16}),
+    ("guard_110_16", "long_b1h32_n16384_d128", "fp4", {"guard": (110, 16)}),
+    ("causal_lse", "long_b1h32_n16384_d128", "fp4", {"causal": True, "lse": True}),
+    ("fp8_pv", "long_b1h32_n16384_d128", "fp4", {"pv_fp8": True}),
+    ("bf16", "long_b1h32_n16384_d128", "bf16", {}),
+    ("online", "outlier_b2h16_n4096_d128", "fp4", {}),
+    ("online", "student_t_b1h32_n8192_d128", "fp4", {}),
+    ("online", "d64_b1h64_n32768", "fp4", {}),
+    ("bf16", "d64_b1h64_n32768", "bf16", {}),
+]
+PASSES = [
+    "SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_VALU_TRANS_F32 SQ_INSTS_VALU_CVT SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_LDS "
+    "SQ_BUSY_CYCLES SQ_WAVE_CYCLES GRBM_GUI_ACTIVE",
+    "SQ_INSTS_VALU_FMA_F32 SQ_ACTIVE_INST_VALU SQ_WAIT_INST_ANY SQ_VALU_MFMA_COEXEC_CYCLES SQ_INSTS_SALU "
+    "SQ_LDS_BANK_CONFLICT SQ_ACTIVE_INST_LDS SQ_WAIT_INST_LDS GRBM_GUI_ACTIVE",
+    "FETCH_SIZE",
+    "WRITE_SIZE",
+]
+N_SIMD = 1024   # 256 CUs x 4 SIMDs
+N_XCD = 8
 
 
-def traffic_summary(fetch_csv, write_csv, out_path=TRAFFIC_FILE):
-    """Write the per-launch HBM traffic file from the counter CSVs of two
-    ``--traffic-run`` passes (FETCH_SIZE, then WRITE_SIZE, in KiB per dispatch).
-    Each counter is scaled by what it reads for the 256 MiB device copy."""
+def _shape_of(inputs):
+    """(B, H, N, d, seed-or-None) of a route's inputs."""
+    import workloads
+    if inputs in workloads.WORKLOADS:
+        w = workloads.WORKLOADS[inputs]
+        return w.B, w.H, w.N, w.d, w
+    d, b, h, n = (int(x[1:]) for x in inputs.split("_"))
+    return b, h, n, d, None
+
+
+def _route_inputs(torch, fa, inputs, cache):
+    """bf16/fp32 q, k, v on the GPU and their MXFP4 operands (cached per inputs)."""
+    if inputs not in cache:
+        import workloads
+        B, H, N, d, w = _shape_of(inputs)
+        if w is not None:
+            q, k, v = (t.cuda() for t in workloads.generate(w))
+        else:
+            g = torch.Generator(device="cuda").manual_seed(21)
+            q, k, v = (torch.randn((B, H, N, d), device="cuda", generator=g).to(torch.bfloat16) for _ in range(3))
+        cache[inputs] = (q, k, v, {})
+    return cache[inputs]
+
+
+def _route_call(torch, fa, label, inputs, family, opts, cache):
+    """A no-argument callable that launches one route's forward (operands prepared)."""
+    q, k, v, ops_cache = _route_inputs(torch, fa, inputs, cache)
+    B, H, N, d, _ = _shape_of(inputs)
+    scale = 1.0 / math.sqrt(d)
+    out = torch.empty((B, H, N, d), dtype=torch.float32, device="cuda")
+    if family == "bf16":
+        return lambda: fa.forward_bf16(q, k, v, softmax_scale=scale, out=out)
+    key = "anchored" if "guard" in opts else ("fp8" if opts.get("pv_fp8") else "plain")
+    if key not in ops_cache:
+        ops_cache[key] = fa.quantize_qkv(q, k, v, anchored=key == "anchored", pv_fp8=key == "fp8")
+    ops = ops_cache[key]
+    kw = dict(opts)
+    if kw.pop("lse", False):
+        kw["lse"] = torch.empty((B, H, N), dtype=torch.float32, device="cuda")
+    return lambda: fa.forward_mxfp4(*ops, softmax_scale=scale, out=out, **kw)
+
+
+def profile_run(torch, fa):
+    """For rocprofv3 passes: a 256 MiB device copy (the traffic counters'
+    calibration), then one launch of every route of PROFILE_ROUTES, in order."""
+    src = torch.empty(64 << 20, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    cache = {}
+    calls = [_route_call(torch, fa, *r, cache) for r in PROFILE_ROUTES]
+    torch.cuda.synchronize()
+    for (label, inputs, family, _), fn in zip(PROFILE_ROUTES, calls):
+        fn()
+        torch.cuda.synchronize()
+        print(f"profile run: {label} on {inputs} ({family}) launched", flush=True)
+
+
+def _route_scores(inputs, opts):
+    """(scores, flop) of one launch: B H N^2 score entries (causal: the visible
+    pairs B H N (N + 1) / 2) and 4 d per score."""
+    B, H, N, d, _ = _shape_of(inputs)
+    scores = B * H * N * (N + 1) / 2 if opts.get("causal") else B * H * N * N
+    return scores, 4.0 * d * scores
+
+
+def counter_summary(out_path, csv_paths):
+    """Write the per-route counter file from the CSVs of the ``--profile-run``
+    passes (PASSES, in order).  Forward-kernel dispatches are matched to
+    PROFILE_ROUTES by dispatch order; the traffic counters are scaled by what they
+    read for the 256 MiB device copy of the same run."""
     import csv
-
-    def per_kernel(path, counter):
-        vals = {}
+    per_pass = []
+    for path in csv_paths:
+        disp = {}
         with open(path) as f:
             for r in csv.DictReader(f):
-                if r["Counter_Name"] == counter:
-                    vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
-        return vals
-
-    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
-
-    def pick(vals, key):
-        hits = [v for k, v in vals.items() if key in k]
-        if len(hits) != 1 or len(hits[0]) != 1:
-            raise SystemExit(f"expected exactly one dispatch of {key!r} in the counter file, got {hits}")
-        return hits[0][0]
-
-    kname = "fwd_mxfp4_kernel<128, 8, false, 0, 0>"
-    copy_bytes = 256 << 20
-    fs = copy_bytes / 1024 / pick(fetch, "copyBuffer")
-    ws = copy_bytes / 1024 / pick(write, "copyBuffer")
-    fk, wk = pick(fetch, kname), pick(write, kname)
-    import workloads
-    w = workloads.WORKLOADS[workloads.BENCH_WORKLOAD]
-    algo = w.B * w.H * (3 * w.N * w.d * (0.5 + 1 / 32) + 4 * w.N * w.d)
-    res = {
-        "kernel": kname,
-        "workload": w.name,
-        "source_sha256": _source_sha(),
-        "fetch_size_kib": fk,
-        "write_size_kib": wk,
-        "copy_calibration": {"bytes": copy_bytes, "fetch_size_kib": pick(fetch, "copyBuffer"),
-                             "write_size_kib": pick(write, "copyBuffer"), "fetch_scale": fs, "write_scale": ws},
-        "fetch_bytes": fk * 1024 * fs,
-        "write_bytes": wk * 1024 * ws,
-        "bytes_per_launch": fk * 1024 * fs + wk * 1024 * ws,
-        "algorithmic_bytes": int(algo),
-        "commands": [
-            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <fetch> -o fetch -- python bench.py --traffic-run",
-            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write> -o write -- python bench.py --traffic-run",
-            "python bench.py --traffic-summary <fetch>/fetch_counter_collection.csv "
-            "<write>/write_counter_collection.csv",
-        ],
-    }
+                d = disp.setdefault(int(r["Dispatch_Id"]), {"kernel": r["Kernel_Name"], "c": {},
+                                                              "vgpr": int(r["VGPR_Count"]),
+                                                              "agpr": int(r["Accum_VGPR_Count"]),
+                                                              "lds": int(r["LDS_Block_Size"]),
+                                                              "scratch": int(r["Scratch_Size"])})
+                d["c"][r["Counter_Name"]] = d["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        order = sorted(disp)
+        fwd = [disp[i] for i in order if "fwd_mxfp4_kernel" in disp[i]["kernel"] or "fwd_bf16_kernel" in disp[i]["kernel"]]
+        copy = [disp[i] for i in order if "copyBuffer" in disp[i]["kernel"]]
+        if len(fwd) != len(PROFILE_ROUTES) or len(copy) != 1:
+            raise SystemExit(f"{path}: {len(fwd)} forward dispatches (expected {len(PROFILE_ROUTES)}), "
+                             f"{len(copy)} copies (expected 1)")
+        per_pass.append((fwd, copy[0]))
+    copy_kib = (256 << 20) / 1024
+    routes = []
+    for i, (label, inputs, family, opts) in enumerate(PROFILE_ROUTES):
+        c = {}
+        for fwd, copy in per_pass:
+            c.update(fwd[i]["c"])
+        k = per_pass[0][0][i]
+        scores, flop = _route_scores(inputs, opts)
+        B, H, N, d, _ = _shape_of(inputs)
+        rec = {"label": label, "inputs": inputs, "family": family, "options": {kk: list(vv) if isinstance(vv, tuple)
+                                                                               else vv for kk, vv in opts.items()},
+               "kernel": k["kernel"].split("(")[0].replace("void ", ""),
+               "vgpr": k["vgpr"], "agpr": k["agpr"], "lds_bytes": k["lds"], "scratch_bytes": k["scratch"],
+               "counters": c, "scores": scores, "flop": flop}
+        der = {}
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in c and "GRBM_GUI_ACTIVE" in c:
+            der["mfma_busy_pct"] = 100.0 * c["SQ_VALU_MFMA_BUSY_CYCLES"] / (c["GRBM_GUI_ACTIVE"] / N_XCD * N_SIMD)
+        if "SQ_INSTS_VALU" in c and "SQ_INSTS_MFMA" in c:
+            der["valu_non_mfma_per_score"] = (c["SQ_INSTS_VALU"] - c["SQ_INSTS_MFMA"]) * 64 / scores
+            der["mfma_per_score"] = c["SQ_INSTS_MFMA"] * 64 / scores
+        for name, key in (("SQ_INSTS_VALU_TRANS_F32", "trans_per_score"), ("SQ_INSTS_VALU_CVT", "cvt_per_score"),
+                          ("SQ_INSTS_VALU_FMA_F32", "fma_f32_per_score"), ("SQ_INSTS_LDS", "lds_insts_per_score"),
+                          ("SQ_INSTS_SALU", "salu_per_score")):
+            if name in c:
+                der[key] = c[name] * 64 / scores
+        if "SQ_WAIT_INST_ANY" in c and "SQ_WAVE_CYCLES" in c:
+            der["wait_inst_any_pct_of_wave_cycles"] = 100.0 * c["SQ_WAIT_INST_ANY"] / c["SQ_WAVE_CYCLES"]
+        if "SQ_LDS_BANK_CONFLICT" in c and "SQ_ACTIVE_INST_LDS" in c and c["SQ_ACTIVE_INST_LDS"]:
+            der["lds_bank_conflict_pct_of_lds_active"] = 100.0 * c["SQ_LDS_BANK_CONFLICT"] / c["SQ_ACTIVE_INST_LDS"]
+        if "FETCH_SIZE" in c and "WRITE_SIZE" in c:
+            fetch_copy = [cp["c"]["FETCH_SIZE"] for _, cp in per_pass if "FETCH_SIZE" in cp["c"]][0]
+            write_copy = [cp["c"]["WRITE_SIZE"] for _, cp in per_pass if "WRITE_SIZE" in cp["c"]][0]
+            der["fetch_bytes"] = c["FETCH_SIZE"] * 1024 * (copy_kib / fetch_copy)
+            der["write_bytes"] = c["WRITE_SIZE"] * 1024 * (copy_kib / write_copy)
+            der["hbm_bytes"] = der["fetch_bytes"] + der["write_bytes"]
+            der["copy_scale"] = {"fetch": copy_kib / fetch_copy, "write": copy_kib / write_copy}
+        if family == "fp4":
+            mx = 1 if opts.get("pv_fp8") else 0.5
+            der["algorithmic_bytes"] = B * H * (N * d * (2 * (0.5 + 1 / 32) + mx + 1 / 32) + 4 * N * d) + (
+                4 * B * H * N if opts.get("lse") else 0)
+        else:
+            der["algorithmic_bytes"] = B * H * (3 * 2 * N * d + 4 * N * d)
+        rec["derived"] = der
+        rec["source_sha256"] = _source_sha(KERNEL_SOURCES if family == "fp4" else BF16_SOURCES)
+        routes.append(rec)
+    res = {"routes": routes, "passes": PASSES,
+           "commands": [f"timeout -s KILL 120 rocprofv3 --pmc {p} --output-format csv -d <dir{i}> -o p{i} -- "
+                        f"python bench.py --profile-run" for i, p in enumerate(PASSES)] +
+                       ["python bench.py --counter-summary " + " ".join(f"<dir{i}>/p{i}_counter_collection.csv"
+                                                                         for i in range(len(PASSES)))]}
     with open(out_path, "w") as f:
         json.dump(res, f, indent=1)
-    print(json.dumps(res))
+    print(json.dumps({"routes": [(r["label"], r["inputs"], r["derived"]) for r in routes]}, indent=1))
+
+
+def _route_counters(label, inputs):
+    """Derived counter figures of a route from the committed counter file, if they
+    were taken on the current source of that route's kernel; else None."""
+    try:
+        with open(COUNTER_FILE) as f:
+            res = json.load(f)
+    except (OSError, ValueError):
+        return None
+    for r in res.get("routes", []):
+        if r["label"] == label and r["inputs"] == inputs:
+            sha = _source_sha(KERNEL_SOURCES if r["family"] == "fp4" else BF16_SOURCES)
+            return dict(r["derived"], kernel=r["kernel"]) if r.get("source_sha256") == sha else None
+    return None
 
 
 def _time_windows(torch, fns, window_ms, windows):
@@ -205,11 +330,11 @@ def paper_shape_sweep(torch, fa, seed=20):
         q, k, v = (torch.randn((1, H, S, d), device="cuda", generator=g, dtype=torch.float32).to(torch.bfloat16)
                    for _ in range(3))
         ops = fa.quantize_qkv(q, k, v)
-        vt = fa.transpose_bf16(v)
+        bf = (q, k, v)
         out = torch.empty((1, H, S, d), dtype=torch.float32, device="cuda")
         scale = 1.0 / math.sqrt(d)
         fns = {"fp4": lambda: fa.forward_mxfp4(*ops, softmax_scale=scale, out=out),
-               "bf16": lambda: fa.forward_bf16(q, k, vt, softmax_scale=scale, out=out)}
+               "bf16": lambda: fa.forward_bf16(*bf, softmax_scale=scale, out=out)}
         for fn in fns.values():
             fn()
         med = _time_windows(torch, fns, 100.0, 3)[0]
@@ -218,46 +343,126 @@ def paper_shape_sweep(torch, fa, seed=20):
                     "bf16_tflops": round(flop / (med["bf16"] * 1e-3) / 1e12, 1),
                     "speedup_vs_bf16": round(med["bf16"] / med["fp4"], 3),
                     "paper_nvmx_tflops": {"gb200": gb200, "b300": b300}})
-        del q, k, v, ops, vt, out
+        del q, k, v, ops, bf, out
     return res
 
 
-def cpu_oracle_baseline(w, q, k, v, budget_s=12.0):
-    """Time the oracle (as it stands) on consecutive rows of head (0, 0) of the bench
-    inputs (CPU tensors q, k, v [B, H, N, d]) until the budget is spent.  Returns the
-    record and the oracle's output rows, for the parity check."""
+def cpu_oracle_baseline(w, q, k, v):
+    """Time the oracle (as it stands) on the workload's seeded sampled query rows
+    (the rows its parity tests check; CPU tensors q, k, v [B, H, N, d]): per
+    (batch, head) its own MXFP4 quantization of K, V and the sampled Q rows, then
+    the Direct-P forward of those rows.  Heads run on a pool of host threads, each
+    with a single-threaded BLAS.  Returns the record and (rows, O) for the parity
+    check of the timed launch."""
     import numpy as np
     import workloads
+    from concurrent.futures import ThreadPoolExecutor
     from oracle import directp, mxfp4
+    blas = "unknown"
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # threadpoolctl missing: report the affinity set
-        threads = len(os.sched_getaffinity(0))
-    q64, k64, v64 = (workloads.as_f64(t[:1, :1])[0, 0] for t in (q, k, v))
+        from threadpoolctl import threadpool_info, threadpool_limits
+        info = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
+    except Exception:  # threadpoolctl missing: BLAS threads as configured
+        threadpool_limits = None
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    rows = workloads.sampled_rows(w)
+    heads = rows // w.N
+
+    def one_head(bh):
+        b, h = divmod(int(bh), w.H)
+        sel = np.nonzero(heads == bh)[0]
+        q64, k64, v64 = (workloads.as_f64(t[b:b + 1, h:h + 1])[0, 0] for t in (q, k, v))
+        qc, qs = mxfp4.quantize(q64[rows[sel] % w.N], axis=-1)
+        kc, ks = mxfp4.quantize(k64, axis=-1)
+        vc, vs = mxfp4.quantize(v64, axis=-2)
+        return sel, directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(sel)), w.softmax_scale,
+                                         want_codes=False)["O"]
+
+    out = np.zeros((len(rows), w.d))
     t0 = time.perf_counter()
-    kc, ks = mxfp4.quantize(k64, axis=-1)
-    vc, vs = mxfp4.quantize(v64, axis=-2)
-    rows_done = 0
-    chunk = 128
-    outs = []
-    while rows_done < w.N and time.perf_counter() - t0 < budget_s:
-        qc, qs = mxfp4.quantize(q64[rows_done:rows_done + chunk], axis=-1)
-        outs.append(directp.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(chunk), w.softmax_scale,
-                                         want_codes=False)["O"])
-        rows_done += chunk
+    limit = threadpool_limits(1, user_api="blas") if threadpool_limits else None
+    try:
+        with ThreadPoolExecutor(max_workers=workers) as ex:
+            for sel, o in ex.map(one_head, np.unique(heads)):
+                out[sel] = o
+    finally:
+        if limit is not None:
+            limit.unregister() if hasattr(limit, "unregister") else None
     dt = time.perf_counter() - t0
-    flops = 4.0 * rows_done * w.N * w.d
+    flops = 4.0 * len(rows) * w.N * w.d
     return {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
-        "cores": int(threads),
+        "cores": workers,
         "kind": "oracle",
-        "sample": f"{rows_done} query rows of head (b0,h0) of {w.name} (all {w.N} keys), "
-                  f"including the oracle's own MXFP4 quantization of that head's K and V; {dt:.1f} s",
+        "sample": f"the {len(rows)} seeded sampled query rows of {w.name} over its {len(np.unique(heads))} heads "
+                  f"(all {w.N} keys), including the oracle's own MXFP4 quantization of each head's K, V and "
+                  f"sampled Q rows; {workers} host threads (one per head at a time, single-threaded BLAS); "
+                  f"{dt:.1f} s",
+        "blas": blas,
         "seconds": round(dt, 2),
-        "full_workload_estimate_s": round(dt * w.rows / rows_done, 1),
-    }, np.concatenate(outs)
+        "full_workload_estimate_s": round(dt * w.rows / len(rows), 1),
+    }, (rows, out)
+
+
+def other_configs(torch, fa, exclude):
+    """The remaining workloads: the forward and the BF16 kernel timed in
+    interleaved windows on each one's own inputs.  The two small ones are
+    launch-bound (microseconds of launch and fill against sub-microsecond
+    matrix work at peak); the two large ones are matrix-bound points with the
+    roofline fraction and, where committed counters match the kernel source,
+    their HBM traffic."""
+    import workloads
+    res = []
+    for name, w in workloads.WORKLOADS.items():
+        if name == exclude:
+            continue
+        q, k, v = (t.cuda() for t in workloads.generate(w))
+        ops = fa.quantize_qkv(q, k, v)
+        out = torch.empty((w.B, w.H, w.N, w.d), dtype=torch.float32, device="cuda")
+        bf = (q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16))
+        fns = {"fp4": lambda: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out),
+               "bf16": lambda: fa.forward_bf16(*bf, softmax_scale=w.softmax_scale, out=out)}
+        for fn in fns.values():
+            fn()
+        med = _time_windows(torch, fns, 100.0, 5)[0]
+        tflops = w.flops / (med["fp4"] * 1e-3) / 1e12
+        rec = {"workload": name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "inputs": f"{w.dist} {w.dtype}",
+               "seed": w.seed, "ms": round(med["fp4"], 5), "tflops": round(tflops, 2),
+               "frac": round(tflops / MXFP4_PEAK_TFLOPS, 4),
+               "bf16_tflops": round(w.flops / (med["bf16"] * 1e-3) / 1e12, 2),
+               "speedup_vs_bf16": round(med["bf16"] / med["fp4"], 3),
+               "us_at_mxfp4_peak": round(w.flops / (MXFP4_PEAK_TFLOPS * 1e12) * 1e6, 4)}
+        if w.flops < 1e10:
+            rec["bound"] = "launch"
+            rec["us_per_launch"] = round(med["fp4"] * 1e3, 3)
+        else:
+            rec["bound"] = "mfma"
+            c = _route_counters("online", name)
+            if c is not None:
+                rec["traffic"] = round(c["hbm_bytes"])
+                rec["algorithmic_bytes"] = c["algorithmic_bytes"]
+                rec["hbm_gbs"] = round(c["hbm_bytes"] / (med["fp4"] * 1e-3) / 1e9, 1)
+                rec["mfma_busy_pct_counters"] = round(c["mfma_busy_pct"], 2)
+            else:
+                rec["traffic"] = None
+        res.append(rec)
+        del q, k, v, ops, out, bf
+    return res
+
+
+def _counter_view(c, ms):
+    """The figures of a route's counter record that the bench line carries."""
+    if c is None:
+        return None
+    keys = ("mfma_busy_pct", "valu_non_mfma_per_score", "trans_per_score", "cvt_per_score", "fma_f32_per_score",
+            "lds_insts_per_score", "wait_inst_any_pct_of_wave_cycles", "hbm_bytes", "algorithmic_bytes")
+    v = {key: (round(c[key], 4) if isinstance(c[key], float) else c[key]) for key in keys if key in c}
+    if "hbm_bytes" in c:
+        v["hbm_gbs"] = round(c["hbm_bytes"] / (ms * 1e-3) / 1e9, 1)
+    return v
 
 
 def main():
@@ -271,14 +476,16 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--no-paper-shapes", action="store_true", help="skip the paper's reported shapes")
-    ap.add_argument("--traffic-run", action="store_true",
-                    help="for rocprofv3 --pmc passes: one 256 MiB device copy (counter calibration), "
-                         "then one forward launch; prints no JSON")
-    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="write the traffic file from the two --traffic-run counter CSVs (no GPU use)")
+    ap.add_argument("--no-other-configs", action="store_true", help="skip the other four workloads")
+    ap.add_argument("--profile-run", action="store_true",
+                    help="for rocprofv3 passes: one 256 MiB device copy (traffic calibration), then one launch "
+                         "of every profiled route; prints no JSON")
+    ap.add_argument("--counter-summary", nargs="+", metavar="CSV",
+                    help="write the per-route counter file from the --profile-run counter CSVs, one per pass "
+                         "in the order of PASSES (no GPU use)")
     args = ap.parse_args()
-    if args.traffic_summary:
-        traffic_summary(*args.traffic_summary)
+    if args.counter_summary:
+        counter_summary(COUNTER_FILE, args.counter_summary)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the forward shards over (batch, head) with no communication "
@@ -289,36 +496,28 @@ def main():
     import workloads
     import paper_2609_04105_amd as fa
 
-    name = args.workload or workloads.BENCH_WORKLOAD
-    w = workloads.WORKLOADS[name]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.profile_run:
+        profile_run(torch, fa)
+        return
+
+    name = args.workload or workloads.BENCH_WORKLOAD
+    w = workloads.WORKLOADS[name]
     q_cpu, k_cpu, v_cpu = workloads.generate(w)
     q, k, v = (t.to(dev) for t in (q_cpu, k_cpu, v_cpu))
     torch.cuda.synchronize()
 
     ops = fa.quantize_qkv(q, k, v)
     out = torch.empty((w.B, w.H, w.N, w.d), dtype=torch.float32, device=dev)
-    q16, k16 = q.to(torch.bfloat16), k.to(torch.bfloat16)
-    vt16 = fa.transpose_bf16(v.to(torch.bfloat16))
+    bf = (q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16))
     out16 = torch.empty_like(out)
-
-    if args.traffic_run:
-        src = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)                      # reads and writes exactly 256 MiB
-        torch.cuda.synchronize()
-        fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out)
-        torch.cuda.synchronize()
-        print(f"traffic run done: copy 268435456 B, one forward on {name}", flush=True)
-        return
 
     def fp4_step():
         fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out)
 
     def bf16_step():
-        fa.forward_bf16(q16, k16, vt16, softmax_scale=w.softmax_scale, out=out16)
+        fa.forward_bf16(*bf, softmax_scale=w.softmax_scale, out=out16)
 
     def quant_step():
         fa.quantize_qkv(q, k, v)
@@ -363,11 +562,13 @@ def main():
     fns["causal"] = lambda: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out, causal=True, lse=lse)
     med.update(_time_windows(torch, fns, 150.0, 3)[0])
     qms, _ = _time_windows(torch, {"quant": quant_step}, 50.0, 3)
+    del ops_anchored, ops8
 
     flops = w.flops
     tflops = flops / (fp4_ms * 1e-3) / 1e12
     bf16_tflops = flops / (med["bf16"] * 1e-3) / 1e12 if "bf16" in med else None
-    traffic = _traffic()
+    c_online = _route_counters("online", name)
+    traffic = round(c_online["hbm_bytes"]) if c_online and "hbm_bytes" in c_online else None
     clk = measured_clock_ghz(torch, fa, ops, w)
     peak_clk = MXFP4_PEAK_TFLOPS * clk / SPEC_CLOCK_GHZ
     stream_blocks = min(1024, ops[0].numel() // (256 * 64))  # 64 operand bytes per thread
@@ -381,13 +582,23 @@ def main():
         "frac": round(tflops / MXFP4_PEAK_TFLOPS, 4),
         "traffic": traffic,
         "kernel": "fwd_mxfp4_kernel<128, 8, false, 0, 0>",
+        "algorithmic_flops_per_launch": flops,
+        "algorithmic_bytes_per_launch": int(w.B * w.H * (3 * w.N * w.d * (0.5 + 1 / 32) + 4 * w.N * w.d)),
+        "counters": _counter_view(c_online, fp4_ms),
         "measured_clock_ghz": round(clk, 3),
         "peak_at_measured_clock": round(peak_clk, 1),
         "frac_at_measured_clock": round(tflops / peak_clk, 4),
         "sustained_mfma_stream": round(stream, 1) if stream else None,
         "frac_of_sustained_mfma_stream": round(tflops / stream, 4) if stream else None,
-        "algorithmic_flops_per_launch": flops,
     }
+
+    def route(label, ms, route_flops, inputs=name, **extra):
+        r = {"ms": round(ms, 5), "tflops": round(route_flops / (ms * 1e-3) / 1e12, 2)}
+        r.update(extra)
+        r["counters"] = _counter_view(_route_counters(label, inputs), ms)
+        return r
+
+    causal_flops = 2.0 * w.d * w.B * w.H * w.N * (w.N + 1)
     line = {
         "metric": "MXFP4 attn fwd TFLOPS (4BHN^2d/t), % MXFP4 MFMA peak, speedup vs BF16",
         "value": round(tflops, 2),
@@ -413,35 +624,40 @@ def main():
         "quantize_qkv_ms": round(qms["quant"], 5),
         "ex2_pairs_sweep": {str(kx): {"ms": round(med[f"ex2_{kx}"], 5),
                                       "tflops": round(flops / (med[f"ex2_{kx}"] * 1e-3) / 1e12, 2),
-                                      "vs_affine": round(med["fp4"] / med[f"ex2_{kx}"], 3)} for kx in EX2_SWEEP},
-        "guard_110_16": {"ms": round(med["guard"], 5), "tflops": round(flops / (med["guard"] * 1e-3) / 1e12, 2),
-                         "vs_online": round(med["fp4"] / med["guard"], 3)},
-        "fp8_pv": {"ms": round(med["fp8pv"], 5), "tflops": round(flops / (med["fp8pv"] * 1e-3) / 1e12, 2),
-                   "vs_mxfp4_pv": round(med["fp4"] / med["fp8pv"], 3)},
+                                      "vs_affine": round(med["fp4"] / med[f"ex2_{kx}"], 3),
+                                      "counters": _counter_view(_route_counters(f"ex2_{kx}", name),
+                                                                med[f"ex2_{kx}"])} for kx in EX2_SWEEP},
+        "guard_110_16": route("guard_110_16", med["guard"], flops, vs_online=round(med["fp4"] / med["guard"], 3)),
+        "fp8_pv": route("fp8_pv", med["fp8pv"], flops, vs_mxfp4_pv=round(med["fp4"] / med["fp8pv"], 3)),
         # visible (query, key) pairs only: 4 d B H N (N + 1) / 2 flop
-        "causal_with_lse": {"ms": round(med["causal"], 5),
-                            "tflops": round(2.0 * w.d * w.B * w.H * w.N * (w.N + 1) / (med["causal"] * 1e-3) / 1e12, 2),
-                            "flops": "4 d B H N (N + 1) / 2"},
+        "causal_with_lse": route("causal_lse", med["causal"], causal_flops, flops="4 d B H N (N + 1) / 2"),
+        "bf16_counters": None if "bf16" not in med else _counter_view(_route_counters("bf16", name), med["bf16"]),
         "wall_ms_timed_region": round(wall_ms, 3),
         "roofline": roof,
         "gpu": torch.cuda.get_device_name(dev),
         "gfx_target": torch.cuda.get_device_properties(dev).gcnArchName,
         "kernel_source_sha256": _source_sha(),
+        "bf16_kernel_source_sha256": _source_sha(BF16_SOURCES),
     }
+    del bf, out16
+    if not args.no_other_configs and not args.no_bf16 and args.workload is None:
+        line["configs"] = other_configs(torch, fa, name)
     if not args.no_paper_shapes and not args.no_bf16:
         line["paper_shapes"] = paper_shape_sweep(torch, fa)
     if not args.no_cpu_baseline:
         import numpy as np
-        line["cpu_baseline"], o_ref = cpu_oracle_baseline(w, q_cpu, k_cpu, v_cpu)
-        # parity of the timed launch on the rows the oracle computed (head (0, 0))
+        line["cpu_baseline"], (rows, o_ref) = cpu_oracle_baseline(w, q_cpu, k_cpu, v_cpu)
+        # parity of the timed launch on the rows the oracle computed
         fp4_step()
         torch.cuda.synchronize()
-        got = out[0, 0, :len(o_ref)].double().cpu().numpy()
+        got = out.reshape(-1, w.d)[torch.from_numpy(rows).to(dev)].double().cpu().numpy()
         rel = float(np.linalg.norm(got - o_ref) / np.linalg.norm(o_ref))
         cos = float(np.sum(got * o_ref) / (np.linalg.norm(got) * np.linalg.norm(o_ref)))
-        line["parity"] = {"rows": int(len(o_ref)), "head": [0, 0], "o_rel_l2": rel, "o_cos": cos,
-                          "gate": {"o_rel_l2_max": 2e-3, "o_cos_min": 0.9999},
-                          "pass": bool(rel <= 2e-3 and cos >= 0.9999)}
+        row_rel = np.linalg.norm(got - o_ref, axis=1) / np.linalg.norm(o_ref, axis=1)
+        line["parity"] = {"rows": int(len(rows)), "row_set": "seeded sampled rows", "o_rel_l2": rel, "o_cos": cos,
+                          "o_worst_row_rel_l2": float(row_rel.max()),
+                          "gate": {"o_rel_l2_max": 2e-3, "o_cos_min": 0.9999, "o_row_rel_l2_max": 2e-3},
+                          "pass": bool(rel <= 2e-3 and cos >= 0.9999 and row_rel.max() <= 2e-3)}
     print(json.dumps(line), flush=True)
 
 

@@ -239,27 +239,17 @@ fp4attn_status fp4attn_forward_mxfp4_ex(const uint8_t* q_codes, const uint8_t* q
  * Same-design BF16 attention forward: the speed baseline of the paper's
  * canonical speedup t_BF16 / t_k (eq. canonical-speedup).  Textbook softmax
  * attention (eq. exact-attention) with the online recurrence
- * (eq. online-recurrence) in base 2, fp32 accumulation and P rounded to bf16
- * for the PV product.
+ * (eq. online-recurrence) in base 2, fp32 accumulation, P rounded to bf16 for
+ * the PV product, and the row sum taken over those same rounded values.
  *
- *   q, k [B, H, N, d] bf16;  vt [B, H, d, N] bf16 (V transposed, see
- *   fp4attn_transpose_bf16);  out [B, H, N, d] of out_dtype.
+ *   q, k, v [B, H, N, d] bf16 (row-major, the same layout for all three);
+ *   out [B, H, N, d] of out_dtype.
  *
  * Errors: as fp4attn_forward_mxfp4 (no affine arguments).
  */
-fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* vt,
+fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* v,
                                     int64_t B, int64_t H, int64_t N, int64_t d,
                                     float softmax_scale, void* out, int out_dtype, void* stream);
-
-/*
- * Layout helper for the BF16 baseline: dst[b, c, r] = src[b, r, c] for
- * `batch` bf16 [rows, cols] matrices.  Not part of the timed forward, like the
- * quantizer.  Errors: INVALID_ARG for null/misaligned pointers, batch/rows/cols
- * < 1, rows or cols not a multiple of 8, batch above 65535 or rows above
- * 65535 * 64.
- */
-fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols,
-                                      void* dst, void* stream);
 
 /*
  * Test hook: runs exactly the forward kernel of fp4attn_forward_mxfp4_ex (same

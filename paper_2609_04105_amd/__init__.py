@@ -23,5 +23,4 @@ from .api import (  # noqa: F401
     quantize_mxfp4,
     quantize_mxfp8,
     quantize_qkv,
-    transpose_bf16,
 )

@@ -29,7 +29,6 @@ SIGNATURES = {
     "fp4attn_quantize_mxfp4_anchored": [_c_p, _int, _i64, _i64, _i64, _int, _i64, _c_p, _c_p, _c_p],
     "fp4attn_forward_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32] * 3 + [_c_p, _int, _c_p],
     "fp4attn_forward_bf16": [_c_p] * 3 + [_i64] * 4 + [_f32, _c_p, _int, _c_p],
-    "fp4attn_transpose_bf16": [_c_p, _i64, _i64, _i64, _c_p, _c_p],
     "fp4attn_forward_options_init": [ctypes.POINTER(ForwardOptions)],
     "fp4attn_forward_mxfp4_ex": [_c_p] * 6 + [_i64] * 4 + [_f32, ctypes.POINTER(ForwardOptions), _c_p, _int, _c_p],
     "fp4attn_debug_directp_mxfp4": [_c_p] * 6 + [_i64] * 4 + [_f32, ctypes.POINTER(ForwardOptions)]

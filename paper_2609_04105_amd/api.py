@@ -242,28 +242,17 @@ def debug_mfma_stream(a_codes, b_codes, blocks, iters):
     return out, blocks * 4 * iters * 4 * 2.0 * 32 * 32 * 64
 
 
-def transpose_bf16(v):
-    """V [..., N, d] bf16 -> V^T [..., d, N] (layout preparation of the BF16 baseline)."""
-    _need(v, "v", torch.bfloat16)
-    lead = tuple(v.shape[:-2])
-    rows, cols = v.shape[-2:]
-    vt = torch.empty(lead + (cols, rows), dtype=torch.bfloat16, device=v.device)
-    _launch(v.device, lib.fp4attn_transpose_bf16, _ptr(v), math.prod(lead) if lead else 1, rows, cols, _ptr(vt),
-            _stream(v))
-    return vt
-
-
-def forward_bf16(q, k, vt, softmax_scale=None, out=None, out_dtype=torch.float32):
-    """Same-design BF16 attention forward; q, k [B, H, N, d], vt [B, H, d, N] bf16."""
+def forward_bf16(q, k, v, softmax_scale=None, out=None, out_dtype=torch.float32):
+    """Same-design BF16 attention forward; q, k, v [B, H, N, d] bf16."""
     _need(q, "q", torch.bfloat16, 4)
     _need(k, "k", torch.bfloat16, 4)
-    _need(vt, "vt", torch.bfloat16, 4)
+    _need(v, "v", torch.bfloat16, 4)
     B, H, N, d = q.shape
-    if tuple(k.shape) != (B, H, N, d) or tuple(vt.shape) != (B, H, d, N):
-        raise ValueError("k must be [B, H, N, d] and vt [B, H, d, N]")
+    if tuple(k.shape) != (B, H, N, d) or tuple(v.shape) != (B, H, N, d):
+        raise ValueError("q, k and v must all be [B, H, N, d]")
     out = _out(out, B, H, N, d, out_dtype, q.device)
-    dev = _same_device(q, k, vt, out)
+    dev = _same_device(q, k, v, out)
     s = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
-    _launch(dev, lib.fp4attn_forward_bf16, _ptr(q), _ptr(k), _ptr(vt), B, H, N, d, s, _ptr(out), _DTYPES[out.dtype],
+    _launch(dev, lib.fp4attn_forward_bf16, _ptr(q), _ptr(k), _ptr(v), B, H, N, d, s, _ptr(out), _DTYPES[out.dtype],
             _stream(out))
     return out

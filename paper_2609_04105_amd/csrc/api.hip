@@ -283,18 +283,18 @@ fp4attn_status fp4attn_debug_directp_mxfp4(const uint8_t* q_codes, const uint8_t
   return from_hip(fp4attn::launch_forward_mxfp4(a, static_cast<hipStream_t>(stream)), "debug forward launch");
 }
 
-fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* vt, int64_t B, int64_t H, int64_t N,
+fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* v, int64_t B, int64_t H, int64_t N,
                                     int64_t d, float softmax_scale, void* out, int out_dtype, void* stream) {
   REQUIRE_PTR(q);
   REQUIRE_PTR(k);
-  REQUIRE_PTR(vt);
+  REQUIRE_PTR(v);
   REQUIRE_PTR(out);
   const fp4attn_status st = check_attention_shape(B, H, N, d, softmax_scale, out_dtype);
   if (st != FP4ATTN_OK) return st;
   fp4attn::Bf16Args a{};
   a.q = q;
   a.k = k;
-  a.vt = vt;
+  a.v = v;
   a.out = out;
   a.B = (int)B;
   a.H = (int)H;
@@ -303,18 +303,6 @@ fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* vt
   a.out_bf16 = out_dtype == FP4ATTN_BF16;
   a.softmax_scale = softmax_scale;
   return from_hip(fp4attn::launch_forward_bf16(a, static_cast<hipStream_t>(stream)), "bf16 forward launch");
-}
-
-fp4attn_status fp4attn_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols, void* dst,
-                                      void* stream) {
-  REQUIRE_PTR(src);
-  REQUIRE_PTR(dst);
-  if (batch < 1 || rows < 1 || cols < 1 || rows % 8 || cols % 8)
-    return fail(FP4ATTN_ERR_INVALID_ARG, "batch, rows, cols must be >= 1 and rows, cols multiples of 8");
-  if (batch > 65535 || (rows + 63) / 64 > 65535)
-    return fail(FP4ATTN_ERR_INVALID_ARG, "batch or rows too large for one launch");
-  return from_hip(fp4attn::launch_transpose_bf16(src, batch, rows, cols, dst, static_cast<hipStream_t>(stream)),
-                  "transpose launch");
 }
 
 fp4attn_status fp4attn_debug_mfma_stream(const uint8_t* a_codes, const uint8_t* b_codes, int blocks, int iters,
@@ -340,6 +328,6 @@ const char* fp4attn_status_string(int status) {
 
 const char* fp4attn_last_error(void) { return g_last_error; }
 
-int fp4attn_abi_version(void) { return (1 << 16) | 4; }
+int fp4attn_abi_version(void) { return (2 << 16) | 0; }
 
 }  // extern "C"

@@ -15,9 +15,6 @@ hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, 
 hipError_t launch_quantize_mxfp8(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
                                  uint8_t* codes, uint8_t* scales, hipStream_t stream);
 
-hipError_t launch_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols, void* dst,
-                                 hipStream_t stream);
-
 struct DirectPArgs {
   const uint8_t* q_codes;
   const uint8_t* q_scales;
@@ -50,7 +47,7 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream);
 struct Bf16Args {
   const void* q;
   const void* k;
-  const void* vt;
+  const void* v;
   void* out;
   int B, H, N, d;
   int out_bf16;

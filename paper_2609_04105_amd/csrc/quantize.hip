@@ -1,4 +1,4 @@
-// MXFP4 and MXFP8 input quantizers and the bf16 transpose used by the BF16 baseline.
+// MXFP4 and MXFP8 input quantizers.
 //
 // Quantizer (eq. mx-scale): per block of 32 values with absolute maximum a,
 // the E8M0 amplitude is 2^floor(log2 a) or 2^ceil(log2 a), whichever has the
@@ -472,25 +472,6 @@ __global__ __launch_bounds__(256) void quantize_mxfp8_bf16_cols_staged_kernel(
   }
 }
 
-// dst[b, c, r] = src[b, r, c] for bf16, through a 64 x 64 LDS tile.
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ src, int64_t rows,
-                                                             int64_t cols, uint16_t* __restrict__ dst) {
-  __shared__ uint16_t tile[64][64 + 2];
-  const int64_t b = blockIdx.z;
-  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
-  const uint16_t* s = src + b * rows * cols;
-  uint16_t* d = dst + b * rows * cols;
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-    const int rr = i / 64, cc = i % 64;
-    if (r0 + rr < rows && c0 + cc < cols) tile[rr][cc] = s[(r0 + rr) * cols + c0 + cc];
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-    const int cc = i / 64, rr = i % 64;
-    if (r0 + rr < rows && c0 + cc < cols) d[(c0 + cc) * rows + r0 + rr] = tile[rr][cc];
-  }
-}
-
 hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,
                                  int64_t n_anchor, uint8_t* codes, uint8_t* scales, hipStream_t stream) {
   const int64_t stride = n_anchor > 0 ? rows / n_anchor : 0;
@@ -560,14 +541,6 @@ hipError_t launch_quantize_mxfp8(const void* src, int src_dtype, int64_t batch, 
       hipLaunchKernelGGL((quantize_mxfp8_kernel<uint16_t, 0>), grid, block, 0, stream, (const uint16_t*)src, batch,
                          rows, cols, codes, scales);
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_bf16(const void* src, int64_t batch, int64_t rows, int64_t cols, void* dst,
-                                 hipStream_t stream) {
-  const dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64), (unsigned)batch), block(256);
-  hipLaunchKernelGGL(transpose_bf16_kernel, grid, block, 0, stream, (const uint16_t*)src, rows, cols,
-                     (uint16_t*)dst);
   return hipGetLastError();
 }
 

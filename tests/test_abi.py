@@ -43,7 +43,7 @@ def test_status_strings(lib):
     assert lib.fp4attn_status_string(0) == b"ok"
     assert lib.fp4attn_status_string(2) == b"unsupported configuration"
     assert lib.fp4attn_status_string(99) == b"unknown status"
-    assert lib.fp4attn_abi_version() >> 16 == 1
+    assert lib.fp4attn_abi_version() >> 16 == 2
 
 
 FAKE = [ctypes.c_void_p(4096 * (i + 1)) for i in range(8)]   # aligned, never dereferenced
@@ -90,8 +90,6 @@ def test_quantize_and_bf16_validation(lib):
     b = lib.fp4attn_forward_bf16
     assert b(*FAKE[:3], 1, 1, 128, 80, 0.125, FAKE[4], 0, None) == 2
     assert b(None, *FAKE[1:3], 1, 1, 128, 64, 0.125, FAKE[4], 0, None) == 1
-    t = lib.fp4attn_transpose_bf16
-    assert t(FAKE[0], 1, 7, 8, FAKE[1], None) == 1
     d = lib.fp4attn_debug_directp_mxfp4
     assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, FAKE[7], -1, *FAKE[:4], None, None) == 1  # n_rows < 0
     assert d(*FAKE[:6], 1, 1, 128, 64, 0.125, None, FAKE[6], 0, FAKE[7], 1, *FAKE[:4], ctypes.c_void_p(4096 + 8),

@@ -1,17 +1,19 @@
 """GPU check of the same-design BF16 baseline against exact fp64 attention
-(eq. exact-attention) on the same bf16 inputs."""
+(eq. exact-attention) on the same bf16 inputs, V taken as [B, H, N, d]."""
 import numpy as np
 import pytest
 import torch
 
 import workloads
 from oracle import exact
-from parity import load_workload, rel_l2_cos
+from parity import load_workload, rel_l2_cos, row_rel_l2
 
 pytestmark = pytest.mark.gpu
 
-# bf16 rounding of P (relative 2^-9 per element) bounds the error well below these
+# bf16 rounding of P (relative 2^-9 per element, and the denominator sums the
+# same rounded values) bounds the error well below these
 REL_MAX = 5e-3
+ROW_REL_MAX = 1e-2
 COS_MIN = 0.99999
 
 
@@ -21,16 +23,15 @@ def fa():
     return fa
 
 
-def _check(fa, host64, dev, rows, label):
+def _check(fa, host64, dev, rows, label, out_dtype=torch.float32):
     q, k, v = host64
     B, H, N, d = q.shape
     s = 1.0 / np.sqrt(d)
     qg, kg, vg = (t.to(torch.bfloat16) for t in dev)
-    vt = fa.transpose_bf16(vg)
-    assert torch.equal(vt, vg.transpose(-1, -2).contiguous())
-    out = fa.forward_bf16(qg, kg, vt)
+    print(f"[bf16 {label}] B{B} H{H} N{N} d{d} rows={len(rows)}", flush=True)
+    out = fa.forward_bf16(qg, kg, vg, out_dtype=out_dtype)
     torch.cuda.synchronize()
-    got = out.reshape(-1, d)[torch.from_numpy(np.asarray(rows)).cuda()].cpu().numpy()
+    got = out.reshape(-1, d)[torch.from_numpy(np.asarray(rows)).cuda()].float().cpu().numpy()
     q16, k16, v16 = (workloads.as_f64(t.cpu()) for t in (qg, kg, vg))
     ref = np.zeros((len(rows), d))
     heads = np.asarray(rows) // N
@@ -39,8 +40,10 @@ def _check(fa, host64, dev, rows, label):
         sel = np.nonzero(heads == bh)[0]
         ref[sel] = exact.attention(q16[b, h][np.asarray(rows)[sel] % N], k16[b, h], v16[b, h], s)
     rel, cos = rel_l2_cos(got, ref)
-    print(f"[bf16 {label}] rel-L2 {rel:.3e} cos {cos:.8f}", flush=True)
-    assert rel <= REL_MAX and cos >= COS_MIN
+    worst = float(row_rel_l2(got, ref).max())
+    print(f"[bf16 {label}] rel-L2 {rel:.3e} cos {cos:.8f} worst row rel-L2 {worst:.3e}", flush=True)
+    assert rel <= REL_MAX and cos >= COS_MIN and worst <= ROW_REL_MAX, (rel, cos, worst)
+    return out
 
 
 def test_bf16_small_all_rows(fa):
@@ -53,17 +56,55 @@ def test_bf16_tiny(fa):
     _check(fa, host64, dev, np.arange(128), "tiny")
 
 
+@pytest.mark.parametrize("N,d,H", [(128, 128, 1), (384, 128, 2), (640, 64, 2), (1152, 128, 3), (512, 128, 128),
+                                   (256, 64, 256)])
+def test_bf16_tiles_all_rows(fa, N, d, H):
+    """One to eighteen 64-key tiles (a tail group of every length), four- and
+    eight-wave workgroups, both head dimensions."""
+    g = torch.Generator().manual_seed(N + d + H)
+    q, k, v = (torch.randn(1, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    rows = np.arange(H * N) if H * N <= 8192 else np.arange(0, H * N, 7)
+    _check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), rows, f"tiles N{N} d{d} H{H}")
+
+
 @pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "long_b1h32_n16384_d128"])
 def test_bf16_full_size_sampled(fa, name):
     host64, dev = load_workload(name)
     _check(fa, host64, dev, workloads.sampled_rows(name)[::4], name)
 
 
-@pytest.mark.parametrize("d", [64, 128])
-def test_bf16_tail_launch(fa, d):
-    """B1 H24 N4096: the four-wave tail launch (384 eight-wave workgroups would
-    leave a half-empty second round); every 97th row checked."""
+@pytest.mark.parametrize("H,d", [(24, 64), (24, 128), (36, 64)])
+def test_bf16_tail_launch(fa, H, d):
+    """B1 N4096 grids whose eight-wave launch would end in a mostly empty round
+    (d = 64 takes four-wave workgroups there); every 97th row checked."""
     g = torch.Generator().manual_seed(10)
-    q, k, v = (torch.randn(1, 24, 4096, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    q, k, v = (torch.randn(1, H, 4096, d, generator=g).to(torch.bfloat16) for _ in range(3))
     host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
-    _check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, 24 * 4096, 97), f"tail d{d}")
+    _check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, H * 4096, 97), f"tail H{H} d{d}")
+
+
+def test_bf16_large_logits_and_bf16_output(fa):
+    """Scores spanning hundreds of binades within a row (the lazy reference
+    rescales many times), and bf16 output equal to the rounded fp32 output."""
+    g = torch.Generator().manual_seed(12)
+    q = (torch.randn(1, 2, 1024, 128, generator=g) * 6).to(torch.bfloat16)
+    k = (torch.randn(1, 2, 1024, 128, generator=g) * 6).to(torch.bfloat16)
+    v = torch.randn(1, 2, 1024, 128, generator=g).to(torch.bfloat16)
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    dev = (q.cuda(), k.cuda(), v.cuda())
+    o32 = _check(fa, host64, dev, np.arange(2048), "large logits")
+    o16 = fa.forward_bf16(*dev, out_dtype=torch.bfloat16)
+    assert torch.equal(o16, o32.to(torch.bfloat16))
+    assert torch.isfinite(o32).all()
+
+
+def test_bf16_deterministic_and_fully_overwritten(fa):
+    g = torch.Generator().manual_seed(13)
+    q, k, v = (torch.randn(1, 4, 512, 64, generator=g).to(torch.bfloat16).cuda() for _ in range(3))
+    o1 = torch.full((1, 4, 512, 64), float("nan"), device="cuda")
+    fa.forward_bf16(q, k, v, out=o1)
+    o2 = torch.full_like(o1, float("nan"))
+    fa.forward_bf16(q, k, v, out=o2)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o1).all() and torch.equal(o1, o2)
