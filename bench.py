@@ -90,7 +90,11 @@ def _shape_of(inputs):
     if inputs in workloads.WORKLOADS:
         w = workloads.WORKLOADS[inputs]
         return w.B, w.H, w.N, w.d, w
-    d, b, h, n = (int(x[1:]) for x in inputs.split("_"))
+    import re
+    m = re.fullmatch(r"d(\d+)_b(\d+)h(\d+)_n(\d+)", inputs)
+    if m is None:
+        raise ValueError(f"unknown route inputs {inputs!r}")
+    d, b, h, n = (int(x) for x in m.groups())
     return b, h, n, d, None
 
 
@@ -152,12 +156,13 @@ def _route_scores(inputs, opts):
     return scores, 4.0 * d * scores
 
 
-def counter_summary(out_path, csv_paths):
+def counter_summary(out_path, csv_paths, routes=None):
     """Write the per-route counter file from the CSVs of the ``--profile-run``
     passes (PASSES, in order).  Forward-kernel dispatches are matched to
     PROFILE_ROUTES by dispatch order; the traffic counters are scaled by what they
     read for the 256 MiB device copy of the same run."""
     import csv
+    routes = PROFILE_ROUTES if routes is None else routes
     per_pass = []
     for path in csv_paths:
         disp = {}
@@ -172,13 +177,13 @@ def counter_summary(out_path, csv_paths):
         order = sorted(disp)
         fwd = [disp[i] for i in order if "fwd_mxfp4_kernel" in disp[i]["kernel"] or "fwd_bf16_kernel" in disp[i]["kernel"]]
         copy = [disp[i] for i in order if "copyBuffer" in disp[i]["kernel"]]
-        if len(fwd) != len(PROFILE_ROUTES) or len(copy) != 1:
-            raise SystemExit(f"{path}: {len(fwd)} forward dispatches (expected {len(PROFILE_ROUTES)}), "
+        if len(fwd) != len(routes) or len(copy) != 1:
+            raise SystemExit(f"{path}: {len(fwd)} forward dispatches (expected {len(routes)}), "
                              f"{len(copy)} copies (expected 1)")
         per_pass.append((fwd, copy[0]))
     copy_kib = (256 << 20) / 1024
-    routes = []
-    for i, (label, inputs, family, opts) in enumerate(PROFILE_ROUTES):
+    records = []
+    for i, (label, inputs, family, opts) in enumerate(routes):
         c = {}
         for fwd, copy in per_pass:
             c.update(fwd[i]["c"])
@@ -220,15 +225,16 @@ def counter_summary(out_path, csv_paths):
             der["algorithmic_bytes"] = B * H * (3 * 2 * N * d + 4 * N * d)
         rec["derived"] = der
         rec["source_sha256"] = _source_sha(KERNEL_SOURCES if family == "fp4" else BF16_SOURCES)
-        routes.append(rec)
-    res = {"routes": routes, "passes": PASSES,
+        records.append(rec)
+    res = {"routes": records, "passes": PASSES,
            "commands": [f"timeout -s KILL 120 rocprofv3 --pmc {p} --output-format csv -d <dir{i}> -o p{i} -- "
                         f"python bench.py --profile-run" for i, p in enumerate(PASSES)] +
                        ["python bench.py --counter-summary " + " ".join(f"<dir{i}>/p{i}_counter_collection.csv"
                                                                          for i in range(len(PASSES)))]}
     with open(out_path, "w") as f:
         json.dump(res, f, indent=1)
-    print(json.dumps({"routes": [(r["label"], r["inputs"], r["derived"]) for r in routes]}, indent=1))
+    print(json.dumps({"routes": [(r["label"], r["inputs"], r["derived"]) for r in records]}, indent=1))
+    return res
 
 
 def _route_counters(label, inputs):

@@ -146,12 +146,14 @@ __device__ __forceinline__ uint2 lds_read_tr16(const uint8_t* p) {
 }
 
 // Two waves per SIMD, except four-wave workgroups with d = 128, whose 128 KiB
-// ring leaves room for one workgroup per CU.
+// ring leaves room for one workgroup per CU, and eight-wave workgroups with
+// d = 64, two per CU (64 KiB of LDS each) at four waves per SIMD (at most 128
+// registers).
 template <int D, int NW>
-constexpr int kMinWaves16 = (D == 128 && NW == 4) ? 1 : 2;
+constexpr int kMinWaves16 = (D == 128 && NW == 4) ? 1 : ((D == 64 && NW == 8) ? 4 : 2);
 
 template <int D, int NW, bool OUT_BF16>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kMinWaves16<D, NW>, 2))) void
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kMinWaves16<D, NW>, kMinWaves16<D, NW> > 2 ? 4 : 2))) void
 fwd_bf16_kernel(const BParams p) {
   using L = BLayout<D>;
   constexpr int BM = NW * 32;
@@ -244,39 +246,22 @@ fwd_bf16_kernel(const BParams p) {
     });
   };
 
+  // Instruction order of one steady-state step (the region before the rescale
+  // branch): the step's V^T reads first, the row-maximum chain while they land,
+  // then every PV and denominator MFMA followed by a slice of the probabilities.
+  constexpr int kStepMfma = 2 * (D / 32) + 2;
   auto schedule_step = [&]() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 8 + 4 * D / 16, 0);  // DS reads: K, V fragments
-    __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);              // VALU: row maximum, reference
-    static_for<D / 16 + D / 16 + 2>([&](auto) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // three VALU of the probabilities
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * (D / 32) * 2, 0);  // DS reads: V^T fragments
+    __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);                // VALU: row maximum
+    static_for<kStepMfma>([&](auto) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                              // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, (40 + kStepMfma - 1) / kStepMfma, 0);  // probabilities
     });
   };
 
-  // Probabilities of step g: row maximum over the step's 32 keys (16 per lane
-  // half, then across the halves), the lazy reference update, and
   // P = 2^(s log2(e) S - M) rounded to bf16 and packed into the two P^T chunk
   // operands (registers 8 c .. 8 c + 7 are keys 16 c + 8 h .. + 7).
-  auto softmax = [&](const v16f& S, v4i (&P)[2], auto SCHED_) {
-    float m = fmaxf(fmaxf(S[0], S[1]), S[2]);
-#pragma unroll
-    for (int r = 3; r < 15; r += 2) m = fmaxf(fmaxf(m, S[r]), S[r + 1]);
-    m = fmaxf(m, S[15]);
-    unsigned ma = as_uint(m), mb = ma;
-    swap_halves(ma, mb);
-    const float y = fmaxf(as_float(ma), as_float(mb)) * p.sc;
-    if (__builtin_amdgcn_ballot_w64(y > Mthr)) {
-      const float Mn = y > Mthr ? floorf(y) : Mref;
-      const int sh = (int)(Mref - Mn);
-#pragma unroll
-      for (int c = 0; c < D / 32; ++c)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
-      Dacc[0] = ldexpf(Dacc[0], sh);
-      Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
-      Mref = Mn;
-      Mthr = Mn + kTau16;
-    }
+  auto probabilities = [&](const v16f& S, v4i (&P)[2]) {
     const float nm = -Mref;
     static_for<2>([&](auto C_) {
       constexpr int c = decltype(C_)::value;
@@ -289,9 +274,38 @@ fwd_bf16_kernel(const BParams p) {
       });
       P[c] = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
     });
+  };
+
+  // Step g's probabilities: row maximum over the step's 32 keys (16 per lane
+  // half, then across the halves) and P with the current reference; only when
+  // the maximum passes the reference by more than tau (a wave-uniform, rare
+  // branch) is the reference raised, O and the denominator rescaled exactly and
+  // P recomputed, so the common path has no branch before the P work.
+  auto softmax = [&](const v16f& S, v4i (&P)[2], auto SCHED_) {
+    float m = fmaxf(fmaxf(S[0], S[1]), S[2]);
+#pragma unroll
+    for (int r = 3; r < 15; r += 2) m = fmaxf(fmaxf(m, S[r]), S[r + 1]);
+    m = fmaxf(m, S[15]);
+    unsigned ma = as_uint(m), mb = ma;
+    swap_halves(ma, mb);
+    const float y = fmaxf(as_float(ma), as_float(mb)) * p.sc;
+    probabilities(S, P);
     // keep the probabilities next to the step's matrix work (emits nothing)
     asm volatile("" ::"v"(P[0]), "v"(P[1]));
     if constexpr (decltype(SCHED_)::value) schedule_step();
+    if (__builtin_amdgcn_ballot_w64(y > Mthr)) {
+      const float Mn = y > Mthr ? floorf(y) : Mref;
+      const int sh = (int)(Mref - Mn);
+#pragma unroll
+      for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) O[c][r] = ldexpf(O[c][r], sh);
+      Dacc[0] = ldexpf(Dacc[0], sh);
+      Dacc[1] = ldexpf(Dacc[1], lane_read(sh, (lane + 16) & 63));  // query lane + 16
+      Mref = Mn;
+      Mthr = Mn + kTau16;
+      probabilities(S, P);
+    }
   };
 
   using Copy = TileCopy16<D, NW>;
@@ -389,14 +403,11 @@ hipError_t launch_forward_bf16(const Bf16Args& a, hipStream_t stream) {
   bp.N = a.N;
   bp.sc = a.softmax_scale * kLog2Ef;
   const int bh = a.B * a.H;
-  // eight-wave (256-query) workgroups when they fill the chip; with d = 64 the
-  // four-wave tail launch of the MXFP4 forward when an eight-wave grid of two to
-  // five rounds would end in a last round at most half full (with d = 128 four
-  // waves would run one wave per SIMD)
+  // d = 128: eight-wave (256-query) workgroups when they fill the chip (four
+  // waves would run one wave per SIMD).  d = 64: eight-wave workgroups, two per
+  // CU, from half a round of them on.
   const int64_t wide_wgs = a.N % 256 == 0 ? (int64_t)(a.N / 256) * bh : 0;
-  const int64_t last_round = wide_wgs % 256;
-  const bool tail = a.d == 64 && wide_wgs > 256 && wide_wgs <= 5 * 256 && last_round != 0 && last_round <= 128;
-  const bool wide = wide_wgs >= 256 && !tail;
+  const bool wide = a.d == 128 ? wide_wgs >= 256 : wide_wgs >= 128;
   const int BM = wide ? 256 : 128;
   bp.n_qtiles = a.N / BM;
   bp.total = bp.n_qtiles * bh;

@@ -270,12 +270,14 @@ struct TileCopy {
 };
 
 // Two waves per SIMD, except where the LDS ring allows one workgroup of four
-// waves per CU only (FP8 V tiles with d = 128: 108 KiB).
+// waves per CU only (FP8 V tiles with d = 128: 108 KiB), and three for
+// four-wave workgroups with d = 64 and FP4 P/V (40 KiB of LDS each, at most
+// 168 registers).
 template <int D, int NW, int VAR>
-constexpr int kMinWaves = ((VAR & kPV8) && NW == 4 && D == 128) ? 1 : 2;
+constexpr int kMinWaves = (VAR & kPV8) ? ((NW == 4 && D == 128) ? 1 : 2) : ((D == 64 && NW == 4) ? 3 : 2);
 
 template <int D, int NW, bool DUMP, int EX2, int VAR>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kMinWaves<D, NW, VAR>, 2))) void
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kMinWaves<D, NW, VAR>, kMinWaves<D, NW, VAR> > 2 ? 3 : 2))) void
 fwd_mxfp4_kernel(const KParams p) {
   constexpr bool PV8 = (VAR & kPV8) != 0;  // FP8 (E4M3) P and V payloads
   constexpr bool GUARD = (VAR & 7) == kVarGuard, CAUSAL = (VAR & 7) == kVarCausal;
