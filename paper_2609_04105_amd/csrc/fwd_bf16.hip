@@ -12,7 +12,7 @@
 //   product, with no cross-lane movement;
 // - K/V tiles of 64 keys in a four-stage LDS ring filled three tiles ahead by
 //   direct-to-LDS buffer loads: K in matrix-operand order, V in its natural
-//   [key][d] layout (16-byte chunks XOR-swizzled by key % 8), read as the V^T
+//   [key][d] layout (16-byte chunks XOR-swizzled by key), read as the V^T
 //   operand by gfx950's transposing LDS read (ds_read_b64_tr_b16), so V is
 //   taken as [B, H, N, d] like Q and K;
 // - a two-deep software pipeline: while the vector ALU turns step g+1 into
@@ -52,6 +52,18 @@ struct BLayout {
   static constexpr int stage = kCodes + vCodes;
 };
 
+// V tiles in LDS: key r's 16-byte chunk c (d = 8 c .. 8 c + 7) sits in slot
+// c ^ swz(r) of its row.  A transposing read of one d block touches 8 rows
+// (r % 16 = 8 h + 4 t + i / 4 over the lanes) and 4 chunks; the swizzle spreads
+// those 32 pieces over all 64 banks, two per 16-byte bank group: for d = 128 (a
+// row is 256 bytes) with the row's low two bits in the slot's high bits and its
+// next two in the low bits; for d = 64 (two rows per 256 bytes) likewise with
+// bit 1 of the row instead of its low two bits.
+template <int D>
+__device__ __forceinline__ int v_swizzle(int r) {
+  return D == 128 ? 4 * (r & 3) + ((r >> 2) & 3) : 4 * ((r >> 1) & 1) + ((r >> 2) & 3);
+}
+
 // Key order of the S^T product within a 32-key step: operand row m = 8 g + 4 h + i
 // holds key 16 (g / 2) + 8 h + 4 (g % 2) + i.  With the 32x32 accumulator layout
 // (row 8 (r / 4) + 4 h + r % 4 in register r of lane half h), register r of lane
@@ -85,7 +97,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_buffer_b(const void* base
 
 // One 64-key tile: K fragments in operand order (item i = one lane's 16 bytes
 // of step s, d chunk c), then V rows in [key][d] order with the 16-byte chunk
-// c of key r stored at chunk slot c ^ (r % 8).  Thread tid copies items
+// c of key r stored at chunk slot c ^ v_swizzle(r).  Thread tid copies items
 // tid, tid + NT, ...; the 64 lanes of a wave copy 64 consecutive items.
 template <int D, int NW>
 struct TileCopy16 {
@@ -118,7 +130,7 @@ struct TileCopy16 {
         off[i] = ((32 * s + key_of_row16(m & 31)) * D + 16 * c + 8 * (m >> 5)) * 2;
       } else {
         const int p = item - nK, r = p / (D / 8), slot = p % (D / 8);
-        off[i] = (r * D + 8 * (slot ^ (r & 7))) * 2;
+        off[i] = (r * D + 8 * (slot ^ v_swizzle<D>(r))) * 2;
       }
     }
   }
@@ -203,12 +215,19 @@ fwd_bf16_kernel(const BParams p) {
   float Mref = -1.0e6f;   // integer row reference (exact in fp32); no key seen yet
   float Mthr = Mref + kTau16;
 
-  // The lane's part of its transposing V reads: lane i of group g = l / 16 reads
-  // key row 8 h + i / 4 (+ 4 t) at d = 16 (g % 2) + 4 (i % 4) (+ 32 cc), i.e. chunk
-  // 2 (g % 2) + (i % 4) / 2 (+ 4 cc), byte 8 (i % 2); with the swizzle the chunk
-  // is XORed with key % 8 = 4 t + i / 4, whose 4 t part combines with 4 cc.
+  // The lane's part of its transposing V reads, one offset per d block cc and key
+  // quarter t: lane i of group g = l / 16 reads key row 8 h + 4 t + i / 4 (plus a
+  // multiple of 16, which leaves the swizzle unchanged) at d = 32 cc + 16 (g % 2) +
+  // 4 (i % 4), i.e. chunk 4 cc + 2 (g % 2) + (i % 4) / 2, byte 8 (i % 2).
   const int gi = lane & 15, gg = (lane >> 4) & 1;
-  const unsigned v_lane = (8 * h + gi / 4) * (2 * D) + 16 * ((2 * gg + (gi & 3) / 2) ^ (gi / 4)) + 8 * (gi & 1);
+  unsigned v_lane[D / 32][2];
+#pragma unroll
+  for (int cc = 0; cc < D / 32; ++cc)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int r = 8 * h + 4 * t + gi / 4;
+      v_lane[cc][t] = r * (2 * D) + 16 * ((4 * cc + 2 * gg + (gi & 3) / 2) ^ v_swizzle<D>(r)) + 8 * (gi & 1);
+    }
 
   const int ntiles = N / kBN16;
   const int nsteps = 2 * ntiles;  // 32-key steps
@@ -234,10 +253,9 @@ fwd_bf16_kernel(const BParams p) {
       constexpr int c = decltype(C_)::value;
       static_for<D / 32>([&](auto CC_) {
         constexpr int cc = decltype(CC_)::value;
-        const uint8_t* base = st + L::vOff + v_lane;
-        constexpr int o0 = (32 * s + 16 * c) * (2 * D) + 64 * (cc ^ 0);
-        constexpr int o1 = (32 * s + 16 * c + 4) * (2 * D) + 64 * (cc ^ 1);
-        const uint2 lo = lds_read_tr16(base + o0), hi = lds_read_tr16(base + o1);
+        constexpr int o = (32 * s + 16 * c) * (2 * D);
+        const uint2 lo = lds_read_tr16(st + L::vOff + o + v_lane[cc][0]);
+        const uint2 hi = lds_read_tr16(st + L::vOff + o + v_lane[cc][1]);
         const v4i vf = {(int)lo.x, (int)lo.y, (int)hi.x, (int)hi.y};
         O[cc] = mfma_bf16_32x32x16(vf, P[c], O[cc]);
       });

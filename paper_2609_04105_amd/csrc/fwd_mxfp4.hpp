@@ -93,7 +93,9 @@ template <int D, bool PV8 = false>
 struct Layout {
   static constexpr int kCodes = (kBN / 32) * (D / 64) * 1024;  // K fragments [sub][chunk][lane][16 B]
   static constexpr int kScales = (kBN / 32) * 64 * 4;          // [sub][lane] u32
-  // V^T fragments [step][chunk][lane][16 B] (FP8: [step][chunk][lane][32 B])
+  // V^T fragments [step][chunk][lane][16 B] (FP8: [step][chunk][half][lane][16 B],
+  // the two 16-byte halves of a lane's 32-byte operand in separate planes, so
+  // each read of a wave is one contiguous 1 KiB)
   static constexpr int vCodes = (kBN / 64) * (D / 32) * (PV8 ? 2048 : 1024);
   static constexpr int vScales = (D / 32) * 64 * 4;            // [chunk][lane] u32
   static constexpr int kOff = 0;
@@ -212,7 +214,7 @@ struct TileCopy {
         // 16 h + [0, 16) (bytes 0-15) and 32 + 16 h + [0, 16) (bytes 16-31) of
         // the 64-key step, while its E8M0 byte still covers keys 32 h + [0, 32).
         const int vi = item - nK;
-        const int hh = vi & 1, m = (vi >> 1) & 63, rest = vi >> 7;
+        const int m = vi & 63, hh = (vi >> 6) & 1, rest = vi >> 7;
         const int cc = rest % (D / 32), s = rest / (D / 32);
         off[i] = (cc * 32 + (m & 31)) * N + s * 64 + (m >> 5) * 16 + hh * 32;
       } else {
@@ -414,7 +416,9 @@ fwd_mxfp4_kernel(const KParams p) {
       constexpr int c = decltype(C_)::value;
       const int vsc = reinterpret_cast<const int*>(st + L::vsOff)[c * 64 + lane];
       if constexpr (PV8) {
-        const v8i vf = *reinterpret_cast<const v8i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 32);
+        const uint8_t* vp = st + L::vOff + (s * (D / 32) + c) * 2048 + lane * 16;
+        const v4i v0 = *reinterpret_cast<const v4i*>(vp), v1 = *reinterpret_cast<const v4i*>(vp + 1024);
+        const v8i vf = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
         O[c] = mfma_fp8_32x32x64<2 * s, 0>(vf, P, O[c], vsc, u);
       } else {
         const v4i vf = *reinterpret_cast<const v4i*>(st + L::vOff + ((s * (D / 32) + c) * 64 + lane) * 16);
