@@ -18,7 +18,7 @@
 // - a two-deep software pipeline: while the vector ALU turns step g+1 into
 //   probabilities, the matrix unit runs PV of step g and QK of step g+2;
 // - an integer row reference with a lazy, exact power-of-two rescale (the
-//   reference may lag the row maximum by up to 8 binades), and the denominator
+//   reference may lag the row maximum by up to 32 binades), and the denominator
 //   from the same bf16 P operand on the matrix unit (an indicator-row
 //   16x16x32 product), so it sums exactly the probabilities PV consumes;
 // - the XCD-aware workgroup order and the launch choice of the MXFP4 forward.
@@ -31,7 +31,7 @@ namespace {
 
 constexpr int kBN16 = 64;       // keys per LDS tile
 constexpr int kStages16 = 4;    // LDS ring depth in tiles
-constexpr float kTau16 = 8.0f;  // lazy rescale threshold in log2 units
+constexpr float kTau16 = 32.0f;  // lazy rescale threshold in log2 units
 constexpr float kLog2Ef = 1.4426950408889634f;
 
 struct BParams {
@@ -296,7 +296,7 @@ fwd_bf16_kernel(const BParams p) {
 
   // Step g's probabilities: row maximum over the step's 32 keys (16 per lane
   // half, then across the halves) and P with the current reference; only when
-  // the maximum passes the reference by more than tau (a wave-uniform, rare
+  // the maximum passes the reference by more than 32 binades (a wave-uniform, rare
   // branch) is the reference raised, O and the denominator rescaled exactly and
   // P recomputed, so the common path has no branch before the P work.
   auto softmax = [&](const v16f& S, v4i (&P)[2], auto SCHED_) {

@@ -58,7 +58,7 @@ namespace fp4attn {
 namespace directp_detail {
 
 constexpr int kBN = 128;   // keys per LDS tile
-constexpr int kTau = 8;    // lazy rescale: the reference may lag the row maximum by up to 8 binades
+constexpr int kTau = 32;   // lazy rescale: the reference may lag the row maximum by up to 32 binades
 constexpr int kStages = 4; // LDS ring depth in tiles
 // Row-reference variants of the kernel: the online integer reference, the
 // sampled guard of Alg. 3, and the online reference with the causal mask;

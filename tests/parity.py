@@ -11,6 +11,7 @@ CODE_MISMATCH_MAX = 1e-4   # fraction of Direct-P codes allowed to differ (round
 O_REL_L2_MAX = 2e-3        # output relative L2 error bound
 O_COS_MIN = 0.9999         # output cosine bound
 O_ROW_REL_L2_MAX = 2e-3    # the same relative L2 bound on every checked row on its own
+TAU = 32                   # the forward's row reference may lag the row maximum by up to TAU binades
 
 
 def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_codes=True, ex2_pairs=0,
@@ -141,7 +142,7 @@ def check_directp_dump(dump, ref, label):
     e_mismatch = float(np.mean(E[seen] != ref["E"][seen]))
     assert e_mismatch <= CODE_MISMATCH_MAX, f"{label}: block exponent mismatch fraction {e_mismatch:.3e}"
     M = dump["row_m"].cpu().numpy().astype(np.int64)
-    assert np.all((M <= ref["M"]) & (M >= ref["M"] - 8)), f"{label}: row reference outside [M - 8, M]"
+    assert np.all((M <= ref["M"]) & (M >= ref["M"] - TAU)), f"{label}: row reference outside [M - {TAU}, M]"
     D = dump["row_d"].cpu().numpy().astype(np.float64) * np.exp2(M - ref["M"])
     rel = np.abs(D - ref["D"]) / ref["D"]
     assert rel.max() < 1e-4, f"{label}: denominator rel error {rel.max():.3e}"
@@ -223,7 +224,7 @@ def check_fp8_dump(dump, ref, label):
     assert np.all(E[~seen] == -32768)
     assert float(np.mean(E[seen] != ref["E"][seen])) <= CODE_MISMATCH_MAX
     M = dump["row_m"].cpu().numpy().astype(np.int64)
-    assert np.all((M <= ref["M"]) & (M >= ref["M"] - 8)), f"{label}: row reference outside [M - 8, M]"
+    assert np.all((M <= ref["M"]) & (M >= ref["M"] - TAU)), f"{label}: row reference outside [M - {TAU}, M]"
     D = dump["row_d"].cpu().numpy().astype(np.float64) * np.exp2(M - ref["M"])
     rel = np.abs(D - ref["D"]) / ref["D"]
     # E4M3 payload sums are not exact in fp32 (E2M1 code sums are): the bound of
