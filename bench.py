@@ -192,7 +192,7 @@ def counter_summary(out_path, csv_paths, routes=None):
         B, H, N, d, _ = _shape_of(inputs)
         rec = {"label": label, "inputs": inputs, "family": family, "options": {kk: list(vv) if isinstance(vv, tuple)
                                                                                else vv for kk, vv in opts.items()},
-               "kernel": k["kernel"].split("(")[0].replace("void ", ""),
+               "kernel": k["kernel"].replace("(anonymous namespace)::", "").split("(")[0].replace("void ", ""),
                "vgpr": k["vgpr"], "agpr": k["agpr"], "lds_bytes": k["lds"], "scratch_bytes": k["scratch"],
                "counters": c, "scores": scores, "flop": flop}
         der = {}
