@@ -263,7 +263,8 @@ fp4attn_status fp4attn_forward_bf16(const void* q, const void* k, const void* v,
  *              ([n_rows, N] E4M3 bytes with pv_fp8)
  *   block_exp  [n_rows, N/32] int16 absolute block exponents E_B (-32768:
  *              the block has no visible key under the causal mask)
- *   row_m      [n_rows] int32 final integer row reference M_i (0 under the guard)
+ *   row_m      [n_rows] int32 final integer row reference M_i (0 under the guard);
+ *              it lags the row's largest block exponent by at most 32 binades
  *   row_d      [n_rows] fp32 represented denominator relative to 2^M_i (under
  *              the guard: sum_B 2^(u'_B - 127) c_B with the published bytes)
  *              (block_exp holds the working exponents ubar_B - 127 under the guard)
