@@ -413,13 +413,46 @@ def cpu_oracle_baseline(w, q, k, v):
     }, (rows, out)
 
 
+def graph_us_per_launch(torch, fns, launches=50, replays=20):
+    """Microseconds per launch of each fn with the host's launch cost taken out:
+    ``launches`` back-to-back calls captured once in a HIP graph (torch.cuda.graph)
+    and replayed; median over ``replays`` timed replays."""
+    res = {}
+    for name, fn in fns.items():
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(launches):
+                fn()
+        graph.replay()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(replays):
+            start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            start.record()
+            graph.replay()
+            end.record()
+            torch.cuda.synchronize()
+            times.append(start.elapsed_time(end) * 1e3 / launches)
+        res[name] = sorted(times)[len(times) // 2]
+        del graph
+    return res
+
+
 def other_configs(torch, fa, exclude):
     """The remaining workloads: the forward and the BF16 kernel timed in
     interleaved windows on each one's own inputs.  The two small ones are
     launch-bound (microseconds of launch and fill against sub-microsecond
     matrix work at peak); the two large ones are matrix-bound points with the
     roofline fraction and, where committed counters match the kernel source,
-    their HBM traffic."""
+    their HBM traffic.  For the launch-bound ones the per-launch time of a
+    captured HIP graph of back-to-back launches is reported beside the
+    per-call time."""
     import workloads
     res = []
     for name, w in workloads.WORKLOADS.items():
@@ -444,6 +477,10 @@ def other_configs(torch, fa, exclude):
         if w.flops < 1e10:
             rec["bound"] = "launch"
             rec["us_per_launch"] = round(med["fp4"] * 1e3, 3)
+            g_us = graph_us_per_launch(torch, fns)
+            rec["graph_us_per_launch"] = {k: round(v, 3) for k, v in g_us.items()}
+            rec["graph_tflops"] = round(w.flops / (g_us["fp4"] * 1e-6) / 1e12, 2)
+            rec["graph_speedup_vs_bf16"] = round(g_us["bf16"] / g_us["fp4"], 3)
         else:
             rec["bound"] = "mfma"
             c = _route_counters("online", name)
