@@ -315,7 +315,8 @@ const char* fp4attn_status_string(int status);
 /* Detail of the last error returned on the calling thread ("" if none). */
 const char* fp4attn_last_error(void);
 
-/* ABI version of this header, (major << 16) | minor. */
+/* ABI version of this header, (major << 16) | minor: 2.0 (fp4attn_forward_bf16
+ * takes V as [B, H, N, d]; 1.x took V transposed). */
 int fp4attn_abi_version(void);
 
 #ifdef __cplusplus

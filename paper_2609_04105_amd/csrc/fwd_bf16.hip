@@ -21,7 +21,8 @@
 //   reference may lag the row maximum by up to 32 binades), and the denominator
 //   from the same bf16 P operand on the matrix unit (an indicator-row
 //   16x16x32 product), so it sums exactly the probabilities PV consumes;
-// - the XCD-aware workgroup order and the launch choice of the MXFP4 forward.
+// - the XCD-aware workgroup order of the MXFP4 forward, and its eight-wave
+//   workgroups at d = 128 (two per CU at four waves per SIMD at d = 64).
 #include "gfx950.hpp"
 #include "launch.hpp"
 

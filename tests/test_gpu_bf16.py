@@ -76,8 +76,9 @@ def test_bf16_full_size_sampled(fa, name):
 
 @pytest.mark.parametrize("H,d", [(24, 64), (24, 128), (36, 64)])
 def test_bf16_tail_launch(fa, H, d):
-    """B1 N4096 grids whose eight-wave launch would end in a mostly empty round
-    (d = 64 takes four-wave workgroups there); every 97th row checked."""
+    """B1 N4096 grids of 384 and 576 eight-wave workgroups, rounds that do not
+    divide the chip (one workgroup per CU at d = 128, two at d = 64); every 97th
+    row checked."""
     g = torch.Generator().manual_seed(10)
     q, k, v = (torch.randn(1, H, 4096, d, generator=g).to(torch.bfloat16) for _ in range(3))
     host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
@@ -108,3 +109,26 @@ def test_bf16_deterministic_and_fully_overwritten(fa):
     fa.forward_bf16(q, k, v, out=o2)
     torch.cuda.synchronize()
     assert torch.isfinite(o1).all() and torch.equal(o1, o2)
+
+
+def test_bf16_longest_sequence_sampled_rows(fa):
+    """N = 2^22 keys, the longest sequence the entry point accepts: one head's K and V
+    take 1 GiB each, so every in-head byte offset of the tile copies is near 2^30.
+    Rows: the first and last of the sequence, of a query tile and of a workgroup,
+    and random ones; inputs drawn on the GPU from a seeded generator."""
+    N, d = 1 << 22, 128
+    g = torch.Generator(device="cuda").manual_seed(24)
+    q, k, v = (torch.randn((1, 1, N, d), device="cuda", generator=g).to(torch.bfloat16) for _ in range(3))
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, N // 2 + 31, N - 257, N - 256, N - 1],
+                                     np.random.default_rng(24).integers(0, N, 8)]))
+    print(f"[bf16 N=2^22] rows={len(rows)}", flush=True)
+    out = fa.forward_bf16(q, k, v)
+    torch.cuda.synchronize()
+    got = out.reshape(-1, d)[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+    q64 = q[0, 0][torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    k64, v64 = (t[0, 0].double().cpu().numpy() for t in (k, v))
+    ref = exact.attention(q64, k64, v64, 1.0 / np.sqrt(d))
+    rel, cos = rel_l2_cos(got, ref)
+    worst = float(row_rel_l2(got, ref).max())
+    print(f"[bf16 N=2^22] rel-L2 {rel:.3e} cos {cos:.8f} worst row rel-L2 {worst:.3e}", flush=True)
+    assert rel <= REL_MAX and cos >= COS_MIN and worst <= ROW_REL_MAX, (rel, cos, worst)
