@@ -1,6 +1,8 @@
 """Throughput of the Direct-P full-MXFP4 attention forward on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py --profile-run                  (one launch per route, for rocprofv3 passes)
+    python bench.py --counter-summary P0 P1 P2 P3  (writes profiles/counters_routes.json)
 
 A step is one forward pass (QK on scaled FP4 matrix cores, Direct-P, PV, the
 epilogue) over the whole workload with MXFP4 operands already resident in HBM;
@@ -14,12 +16,15 @@ inputs (windows interleaved with the FP4 ones, the paper's speedup
 t_BF16 / t_FP4), the roofline of the forward kernel against the dense MXFP4
 matrix peak (and, beside it, the shader clock the kernel ran at and the rate
 a stream of FP4 matrix products alone sustains on the workload's K and Q
-codes), both kernels on the shapes the paper reports (D128 and D64) next to
-the paper's printed rates, and the CPU oracle timed on a
-bounded sample of rows.  The
-defaults follow the paper's timing protocol (Sec. "Operator benchmark suites"): 240
-warmup steps (over 300 ms), 2200 timed steps (about 3 s), and ten interleaved
-300 ms windows of each of the FP4 and BF16 kernels.
+codes), HBM traffic and hardware-counter figures per route from the committed
+counter file (only while it matches the kernel sources), the other routes
+(native-exponential pairs, the sampled guard, FP8 P/V, causal with LSE), the
+other four workloads, both kernels on the shapes the paper reports (D128 and
+D64) next to the paper's printed rates, and the CPU oracle timed on the
+workload's sampled rows.  The defaults follow the paper's timing protocol (Sec.
+"Operator benchmark suites"): 240 warmup steps (over 300 ms), 2200 timed steps
+(about 3 s), and ten interleaved 300 ms windows of each of the FP4 and BF16
+kernels.
 """
 import argparse
 import hashlib
