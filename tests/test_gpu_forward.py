@@ -102,13 +102,14 @@ def test_half_round_tail_launch(fa, H, d):
     _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), np.arange(0, B * H * N, 23), f"tail H{H} d{d}")
 
 
-@pytest.mark.parametrize("name", ["small_b1h8_n1024_d64", "long_b1h32_n16384_d128"])
+@pytest.mark.parametrize("name", ["small_b1h8_n1024_d64", "outlier_b2h16_n4096_d128", "student_t_b1h32_n8192_d128",
+                                  "long_b1h32_n16384_d128"])
 def test_codes_against_plain_fp64_map(fa, name):
     """The GPU's Direct-P codes and block exponents against the code map of eq.
     affine-code-map written out in fp64 (the oracle's ``affine64`` mode: y = z log2 e,
     E_B = floor(max y), q = Q_E2M1(max(0, A (y - E_B + log2 6) + B)), no fp32
     folding of the coefficients), at the same 1e-4 gate; all rows of the small
-    workload, the 4096 sampled rows of the long one.  The output is held to the
+    workload, the 4096 sampled rows of the outlier, Student-t and long ones.  The output is held to the
     fp64 map's output too.  Both mismatch fractions are printed: against the fp64
     map and against the oracle's fp32 fused multiply-add decision."""
     (q, k, v), dev = load_workload(name)
