@@ -30,18 +30,29 @@ def oracle_rows(q, k, v, rows, softmax_scale, affine_a=1.5, affine_b=1.2, want_c
            "M": np.zeros(len(rows), dtype=np.int64), "D": np.zeros(len(rows)), "LSE": np.zeros(len(rows))}
     if want_codes:
         out["codes"] = np.zeros((len(rows), N), dtype=np.uint8)
-    for bh in np.unique(heads):
+
+    def one_head(bh):
         b, h = divmod(int(bh), H)
         sel = np.nonzero(heads == bh)[0]
         local = rows[sel] % N
         qc, qs = mxfp4.quantize(q[b, h], axis=-1)
         kc, ks = mxfp4.quantize(k[b, h], axis=-1)
         vc, vs = mxfp4.quantize(v[b, h], axis=-2)
-        res = directp.forward_rows(qc, qs, kc, ks, vc, vs, local, softmax_scale, affine_a, affine_b, mode=mode,
-                                   want_codes=want_codes, ex2_pairs=ex2_pairs, causal=causal)
+        return sel, directp.forward_rows(qc, qs, kc, ks, vc, vs, local, softmax_scale, affine_a, affine_b, mode=mode,
+                                         want_codes=want_codes, ex2_pairs=ex2_pairs, causal=causal)
+
+    for sel, res in _per_head(one_head, heads):
         for key in res:
             out[key][sel] = res[key]
     return out
+
+
+def _per_head(fn, heads, workers=8):
+    """fn(bh) for every head in ``heads``, on a pool of host threads (the oracle's
+    NumPy work releases the interpreter lock), in head order."""
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        return list(ex.map(fn, np.unique(heads)))
 
 
 def oracle_rows_two_maps(q, k, v, rows, softmax_scale, workers=8):
@@ -49,7 +60,6 @@ def oracle_rows_two_maps(q, k, v, rows, softmax_scale, workers=8):
     decisions of the oracle, from one quantization of each head: ``affine64``
     (eq. affine-code-map written out in fp64, with its output O) and
     ``affine32`` (the fp32 fused multiply-add).  Heads run on a thread pool."""
-    from concurrent.futures import ThreadPoolExecutor
     B, H, N, d = q.shape
     rows = np.asarray(rows, dtype=np.int64)
     heads = rows // N
@@ -69,10 +79,9 @@ def oracle_rows_two_maps(q, k, v, rows, softmax_scale, workers=8):
         E32, _, k32 = directp.block_exponents_and_codes(raw, softmax_scale, 1.5, 1.2, "affine32")
         return sel, res, E32, k32
 
-    with ThreadPoolExecutor(max_workers=workers) as ex:
-        for sel, res, E32, k32 in ex.map(one_head, np.unique(heads)):
-            out["codes64"][sel], out["E64"][sel], out["O64"][sel] = res["codes"], res["E"], res["O"]
-            out["codes32"][sel], out["E32"][sel] = k32, E32
+    for sel, res, E32, k32 in _per_head(one_head, heads, workers):
+        out["codes64"][sel], out["E64"][sel], out["O64"][sel] = res["codes"], res["E"], res["O"]
+        out["codes32"][sel], out["E32"][sel] = k32, E32
     return out
 
 
@@ -160,15 +169,17 @@ def oracle_rows_guarded(q, k, v, rows, softmax_scale, margin, shift, ex2_pairs=0
     heads = rows // N
     out = {"O": np.zeros((len(rows), d)), "ebar": np.zeros((len(rows), N // 32), dtype=np.int64),
            "D": np.zeros(len(rows)), "LSE": np.zeros(len(rows)), "codes": np.zeros((len(rows), N), dtype=np.uint8)}
-    for bh in np.unique(heads):
+    def one_head(bh):
         b, h = divmod(int(bh), H)
         sel = np.nonzero(heads == bh)[0]
         local = rows[sel] % N
         qc, qs = mxfp4.quantize(q[b, h][local], axis=-1)
         kc, ks = mxfp4.quantize(k[b, h][perm], axis=-1)
         vc, vs = mxfp4.quantize(v[b, h][perm], axis=-2)
-        res = guard.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(local)), softmax_scale, margin, shift,
-                                 ex2_pairs=ex2_pairs)
+        return sel, guard.forward_rows(qc, qs, kc, ks, vc, vs, np.arange(len(local)), softmax_scale, margin, shift,
+                                       ex2_pairs=ex2_pairs)
+
+    for sel, res in _per_head(one_head, heads):
         for key in out:
             out[key][sel] = res[key]
     return out
@@ -200,13 +211,15 @@ def oracle_rows_fp8(q, k, v, rows, softmax_scale, causal=False):
     out = {"O": np.zeros((len(rows), d)), "E": np.zeros((len(rows), N // 32), dtype=np.int64),
            "M": np.zeros(len(rows), dtype=np.int64), "D": np.zeros(len(rows)), "LSE": np.zeros(len(rows)),
            "codes": np.zeros((len(rows), N), dtype=np.uint8)}
-    for bh in np.unique(heads):
+    def one_head(bh):
         b, h = divmod(int(bh), H)
         sel = np.nonzero(heads == bh)[0]
         qc, qs = mxfp4.quantize(q[b, h], axis=-1)
         kc, ks = mxfp4.quantize(k[b, h], axis=-1)
         vc, vs = fp8pv.quantize(v[b, h], axis=-2)
-        res = fp8pv.forward_rows(qc, qs, kc, ks, vc, vs, rows[sel] % N, softmax_scale, causal=causal)
+        return sel, fp8pv.forward_rows(qc, qs, kc, ks, vc, vs, rows[sel] % N, softmax_scale, causal=causal)
+
+    for sel, res in _per_head(one_head, heads):
         for key in out:
             out[key][sel] = res[key]
     return out

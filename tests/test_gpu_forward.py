@@ -272,6 +272,13 @@ def test_affine_variant_and_scale(fa):
     _run_and_check(fa, host64, dev, np.arange(2 * 1024), "wan affine", softmax_scale=0.2, affine=(1.6, 0.95))
 
 
+def test_affine_variant_long_sampled_rows(fa):
+    """The Wan fit on the long workload's 4096 sampled rows (the timed launch shape)."""
+    name = "long_b1h32_n16384_d128"
+    host64, dev = load_workload(name)
+    _run_and_check(fa, host64, dev, workloads.sampled_rows(name), f"{name} wan affine", affine=(1.6, 0.95))
+
+
 def test_extreme_logits_stay_finite(fa):
     """Rows whose log2 range exceeds the E8M0 byte range (zero blocks, reference jumps)."""
     g = torch.Generator().manual_seed(11)
@@ -414,9 +421,9 @@ def test_ex2_mixing_small_all_rows(fa, ex2_pairs):
                    ex2_pairs=ex2_pairs)
 
 
-@pytest.mark.parametrize("ex2_pairs", [4, 16])
-def test_ex2_mixing_long_sampled_rows(fa, ex2_pairs):
-    name = "long_b1h32_n16384_d128"
+@pytest.mark.parametrize("name,ex2_pairs", [("long_b1h32_n16384_d128", 4), ("long_b1h32_n16384_d128", 16),
+                                            ("outlier_b2h16_n4096_d128", 4), ("student_t_b1h32_n8192_d128", 4)])
+def test_ex2_mixing_large_sampled_rows(fa, name, ex2_pairs):
     host64, dev = load_workload(name)
     _run_and_check(fa, host64, dev, workloads.sampled_rows(name), f"{name} ex2={ex2_pairs}", ex2_pairs=ex2_pairs)
 
@@ -494,7 +501,7 @@ def test_guard_with_native_exponential_pairs(fa, ex2_pairs):
     _run_guarded(fa, host64, dev, workloads.sampled_rows("small_b1h8_n1024_d64"), "small", 110, 16, ex2_pairs)
 
 
-@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "long_b1h32_n16384_d128"])
+@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "student_t_b1h32_n8192_d128", "long_b1h32_n16384_d128"])
 def test_guard_full_size_sampled_rows(fa, name):
     host64, dev = load_workload(name)
     _run_guarded(fa, host64, dev, workloads.sampled_rows(name), name, 110, 16)
@@ -567,8 +574,8 @@ def test_causal_tiles_all_rows(fa, N, d, H):
     _run_and_check(fa, host64, (q.cuda(), k.cuda(), v.cuda()), rows, f"causal N{N} d{d} H{H}", causal=True, lse=True)
 
 
-def test_causal_long_sampled_rows(fa):
-    name = "long_b1h32_n16384_d128"
+@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "student_t_b1h32_n8192_d128", "long_b1h32_n16384_d128"])
+def test_causal_large_sampled_rows(fa, name):
     host64, dev = load_workload(name)
     _run_and_check(fa, host64, dev, workloads.sampled_rows(name), f"causal {name}", causal=True, lse=True)
 
@@ -652,7 +659,7 @@ def test_fp8pv_tiles(fa, N, d, H):
     _run_fp8(fa, host64, (q.cuda(), k.cuda(), v.cuda()), rows, f"N{N} d{d} H{H}", causal=(N == 384))
 
 
-@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "long_b1h32_n16384_d128"])
+@pytest.mark.parametrize("name", ["outlier_b2h16_n4096_d128", "student_t_b1h32_n8192_d128", "long_b1h32_n16384_d128"])
 def test_fp8pv_full_size_sampled_rows(fa, name):
     host64, dev = load_workload(name)
     _run_fp8(fa, host64, dev, workloads.sampled_rows(name), name)
