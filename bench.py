@@ -66,6 +66,8 @@ def _source_sha(paths=None):
 # workload name or a paper shape "d64_b1h64_n32768" (N(0, 1) bf16 drawn on the GPU).
 PROFILE_ROUTES = [
     ("online", "long_b1h32_n16384_d128", "fp4", {}),
+    ("ex2_1", "long_b1h32_n16384_d128", "fp4", {"ex2_pairs": 1}),
+    ("ex2_2", "long_b1h32_n16384_d128", "fp4", {"ex2_pairs": 2}),
     ("ex2_4", "long_b1h32_n16384_d128", "fp4", {"ex2_pairs": 4}),
     ("ex2_16", "long_b1h32_n16384_d128", "fp4", {"ex2_pairs": 16}),
     ("guard_110_16", "long_b1h32_n16384_d128", "fp4", {"guard": (110, 16)}),
