@@ -136,8 +136,16 @@ fp4attn_status fp4attn_quantize_mxfp4_anchored(const void* src, int src_dtype, i
  * N % 128 != 0, softmax_scale not finite or <= 0, affine_a not finite or <= 0,
  * affine_b not finite, bad out_dtype, B*H*N beyond 2^31 - 1 or B*H beyond
  * 16776960 (65535 * 256).  UNSUPPORTED for
- * d not in {64, 128} or N above 4194304 (2^22) keys.  Non-finite operands (E8M0 byte 255) give unspecified but
- * non-faulting results for the rows they touch.
+ * d not in {64, 128} or N above 4194304 (2^22) keys.
+ *
+ * Non-finite inputs (a block whose E8M0 byte is 255, as the quantizers write for a
+ * block holding NaN or +-Inf; the matrix unit reads that byte as NaN) never fault
+ * and stay within their head: a non-finite Q block makes every score of its row
+ * NaN, every code of the row 0 and the output row NaN (0/0); a non-finite K block
+ * makes its key's score NaN in every row, which the code map sends to code 0 and
+ * the block maximum skips, so each row is the forward over the other keys; a
+ * non-finite V^T block (32 keys of one column) makes that column NaN in every row
+ * of the head.  The extended routes promise only that they do not fault.
  */
 fp4attn_status fp4attn_forward_mxfp4(const uint8_t* q_codes, const uint8_t* q_scales,
                                      const uint8_t* k_codes, const uint8_t* k_scales,

@@ -688,3 +688,53 @@ def test_fp8pv_fidelity_against_exact_attention(fa):
     print(f"[fidelity] MXFP4 P/V cos {m4[0]:.6f} rel-L2 {m4[1]:.6f}; FP8 P/V cos {m8[0]:.6f} rel-L2 {m8[1]:.6f}",
           flush=True)
     assert m8[0] > 0.98 and m8[1] < 0.55 * m4[1]
+
+
+
+@pytest.mark.parametrize("where", ["q_row", "k_key", "v_column"])
+def test_non_finite_input_propagation(fa, where):
+    """A NaN in one input element (its 32-value block gets E8M0 byte 255, which the
+    matrix unit reads as NaN) propagates as the header states, and nothing else moves:
+    * Q row 5 of head 0: every score of that row is NaN, every code 0, the output row
+      NaN (0/0); every other row matches the oracle.
+    * K key 77 of head 1: that key's score is NaN in every row, so its code is 0 and it
+      sets no block maximum: head 1 equals the oracle run with key 77 moved far below
+      every other score (K row 77 = -1024 e_10 against queries whose element 10 is at
+      least 1/2), which gives the key code 0 by the code map.
+    * V element (77, 10) of head 1: column 10 of every row of head 1 is NaN (the V^T
+      block of keys 64..95 in that column is NaN); all other columns, and head 0, match
+      the oracle run with that element set to 0."""
+    g = torch.Generator().manual_seed(40)
+    B, H, N, d = 1, 2, 256, 64
+    q, k, v = (torch.randn(B, H, N, d, generator=g) for _ in range(3))
+    q[0, 1, :, 10] = q[0, 1, :, 10].abs() + 0.5
+    q_ref, k_ref, v_ref = q.clone(), k.clone(), v.clone()
+    nan_rows = np.zeros(B * H * N, dtype=bool)
+    nan_cols = np.zeros((B * H * N, d), dtype=bool)
+    if where == "q_row":
+        q[0, 0, 5, 3] = float("nan")
+        nan_rows[5] = True
+        nan_cols[5] = True
+    elif where == "k_key":
+        k[0, 1, 77, 10] = float("nan")
+        k_ref[0, 1, 77] = 0.0
+        k_ref[0, 1, 77, 10] = -1024.0
+    else:
+        v[0, 1, 77, 10] = float("nan")
+        v_ref[0, 1, 77, 10] = 0.0
+        nan_cols[N:, 10] = True
+    q, k, v, q_ref, k_ref, v_ref = (t.to(torch.bfloat16) for t in (q, k, v, q_ref, k_ref, v_ref))
+    print(f"[non-finite {where}] B{B} H{H} N{N} d{d}", flush=True)
+    out = fa.forward_mxfp4(*gpu_operands(q.cuda(), k.cuda(), v.cuda()))
+    torch.cuda.synchronize()
+    got = out.reshape(-1, d).cpu().numpy().astype(np.float64)
+    print(f"[non-finite {where}] NaN entries {int(np.isnan(got).sum())}, expected {int(nan_cols.sum())}", flush=True)
+    assert np.array_equal(np.isnan(got), nan_cols), "NaN entries differ from the documented propagation"
+    host64 = tuple(workloads.as_f64(t) for t in (q_ref, k_ref, v_ref))
+    rows = np.nonzero(~nan_rows)[0]
+    ref = oracle_rows(*host64, rows, 1.0 / np.sqrt(d), want_codes=False)
+    keep = ~nan_cols[rows]
+    cols = np.nonzero(keep.all(axis=0))[0]          # columns finite in every checked row
+    check_output(got[rows][:, cols], ref["O"][:, cols], f"non-finite {where}, finite entries")
+    if where == "v_column":
+        check_output(got[:N], ref["O"][:N], "non-finite v_column, head 0 all columns")
