@@ -259,6 +259,38 @@ def _route_counters(label, inputs):
     return None
 
 
+def quantizer_roofline(torch, fa, qkv, qkv_ms):
+    """HBM roofline of the input quantizer (outside the timed forward, as in the
+    paper).  Algorithmic bytes per element: the bf16 input read once (2) and the
+    E2M1 code (1/2) plus 1/32 of an E8M0 byte written.  Each kernel is timed on Q,
+    K and V in turn (three tensors, more than the 256 MB Infinity Cache when each
+    is as large as the long workload's), so every call reads its input from HBM:
+    the rows kernel (blocks along d: Q and K) and the V^T kernel (blocks along the
+    sequence, transposed output)."""
+    n = qkv[0].numel()
+    per_elem = 2 + 0.5 + 1 / 32
+    if qkv[0].dtype != torch.bfloat16:
+        return None
+    turn = {"rows": 0, "vt": 0}
+
+    def call(axis, key):
+        x = qkv[turn[key] % 3]
+        turn[key] += 1
+        fa.quantize_mxfp4(x, axis=axis)
+
+    med, _ = _time_windows(torch, {"rows": lambda: call(-1, "rows"), "vt": lambda: call(-2, "vt")}, 50.0, 5)
+
+    def entry(us, nbytes):
+        gbs = nbytes / (us * 1e-6) / 1e9
+        return {"us": round(us, 2), "algorithmic_bytes": int(nbytes), "achieved": round(gbs, 1),
+                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+    return {"bound": "hbm", "peak": HBM_PEAK_GBS, "unit": "GB/s", "bytes_per_element": per_elem,
+            "rows_kernel": entry(med["rows"] * 1e3, n * per_elem),
+            "vt_kernel": entry(med["vt"] * 1e3, n * per_elem),
+            "quantize_qkv": entry(qkv_ms * 1e3, 3 * n * per_elem)}
+
+
 def _time_windows(torch, fns, window_ms, windows):
     """Median per-call ms of each fn over ``windows`` interleaved windows of about
     ``window_ms`` each (calls per window from a one-call estimate), timed with events
@@ -612,6 +644,7 @@ def main():
     fns["causal"] = lambda: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out, causal=True, lse=lse)
     med.update(_time_windows(torch, fns, 150.0, 3)[0])
     qms, _ = _time_windows(torch, {"quant": quant_step}, 50.0, 3)
+    quantizer = quantizer_roofline(torch, fa, (q, k, v), qms["quant"])
     del ops_anchored, ops8
 
     flops = w.flops
@@ -672,6 +705,7 @@ def main():
         "fp4_ms_median_interleaved": round(med["fp4"], 5),
         "bf16_ms_median_interleaved": None if "bf16" not in med else round(med["bf16"], 5),
         "quantize_qkv_ms": round(qms["quant"], 5),
+        "quantizer": quantizer,
         "ex2_pairs_sweep": {str(kx): {"ms": round(med[f"ex2_{kx}"], 5),
                                       "tflops": round(flops / (med[f"ex2_{kx}"] * 1e-3) / 1e12, 2),
                                       "vs_affine": round(med["fp4"] / med[f"ex2_{kx}"], 3),

@@ -292,19 +292,35 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_kernel(const uin
   *reinterpret_cast<v4i*>(codes + ((col0 + 1) * nblk + blk) * 16) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
 }
 
+// The E8M0 bytes of blocks 8 grp .. 8 grp + 7 of one column (byte l of `run` is
+// block 8 grp + l) to `dst`: one 8-byte store when every column has whole groups
+// of 8 blocks (dst is then 8-byte aligned), else one byte per block that exists.
+__device__ __forceinline__ void store_scale_run(uint8_t* dst, uint2 run, int64_t nblk, int64_t grp) {
+  if (nblk % 8 == 0) {
+    *reinterpret_cast<uint2*>(dst) = run;
+  } else {
+    const uint64_t bytes = ((uint64_t)run.y << 32) | run.x;
+    for (int l = 0; l < 8 && grp * 8 + l < nblk; ++l) dst[l] = (uint8_t)(bytes >> (8 * l));
+  }
+}
+
 // bf16, blocks along rows with transposed output (V), staged: a workgroup takes
 // 64 columns x 256 rows (32 column pairs x 8 blocks; a thread quantizes one block
 // of two adjacent columns as above), parks its codes and scale bytes in LDS, and
-// writes each column's 8 blocks of codes as one contiguous 128-byte run.  The
-// loads stay 128-byte row segments.  cols % 64 == 0; blocks past the last are
-// skipped (their threads still meet the barrier).
+// writes each column's 8 blocks of codes as one contiguous 128-byte run (each
+// store instruction of a wave covers 64 contiguous bytes of 16 columns) and its 8
+// scale bytes with one store.  The loads stay 128-byte row segments; the
+// workgroups that take the column groups of the same rows are launched next to
+// each other, so the wider rows of d = 128 are read whole at about the same
+// time.  cols % 64 == 0; blocks past the last are skipped (their threads still
+// meet the barrier).
 __global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_staged_kernel(
     const uint16_t* __restrict__ src, int64_t batch, int64_t rows, int64_t cols, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales, int64_t n_anchor, int64_t anchor_stride) {
   __shared__ uint4 code_lds[64][8];
-  __shared__ uint8_t scale_lds[64][8];
+  __shared__ uint2 scale_lds[64];  // 8 bytes per column
   const int64_t nblk = rows / 32, ngrp = (nblk + 7) / 8, ncg = cols / 64;
-  const int64_t grp = blockIdx.x % ngrp, cg = (blockIdx.x / ngrp) % ncg, b = blockIdx.x / (ngrp * ncg);
+  const int64_t cg = blockIdx.x % ncg, grp = (blockIdx.x / ncg) % ngrp, b = blockIdx.x / (ngrp * ncg);
   const int tid = threadIdx.x, cp = tid % 32, lb = tid / 32;
   const int64_t blk = grp * 8 + lb;
   if (blk < nblk) {
@@ -320,25 +336,23 @@ __global__ __launch_bounds__(256) void quantize_mxfp4_bf16_cols_staged_kernel(
       raw1[i] = (pair[2 * i] >> 16) | (pair[2 * i + 1] & 0xffff0000u);
     }
     unsigned w[4];
-    scale_lds[2 * cp][lb] = (uint8_t)mxfp4_block_bf16(raw0, w);
+    uint8_t* sb = reinterpret_cast<uint8_t*>(scale_lds);
+    sb[16 * cp + lb] = (uint8_t)mxfp4_block_bf16(raw0, w);
     code_lds[2 * cp][lb] = uint4{w[0], w[1], w[2], w[3]};
-    scale_lds[2 * cp + 1][lb] = (uint8_t)mxfp4_block_bf16(raw1, w);
+    sb[16 * cp + 8 + lb] = (uint8_t)mxfp4_block_bf16(raw1, w);
     code_lds[2 * cp + 1][lb] = uint4{w[0], w[1], w[2], w[3]};
   }
   __syncthreads();
-  // thread t writes blocks 2 (t % 4) and 2 (t % 4) + 1 of column t / 4
+  // thread t writes blocks (t % 4) and (t % 4) + 4 of column t / 4
   const int c = tid / 4, part = tid % 4;
   const int64_t col = b * cols + cg * 64 + c;
   uint8_t* cdst = codes + (col * nblk + grp * 8) * 16;
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
-    const int l = 2 * part + k;
+    const int l = part + 4 * k;
     if (grp * 8 + l < nblk) *reinterpret_cast<uint4*>(cdst + l * 16) = code_lds[c][l];
   }
-  if (tid < 64) {
-    const int64_t colx = b * cols + cg * 64 + tid;
-    for (int l = 0; l < 8 && grp * 8 + l < nblk; ++l) scales[colx * nblk + grp * 8 + l] = scale_lds[tid][l];
-  }
+  if (tid < 64) store_scale_run(scales + (b * cols + cg * 64 + tid) * nblk + grp * 8, scale_lds[tid], nblk, grp);
 }
 
 // MXFP8 (E4M3 payload + E8M0 per 32 values): the amplitude is the smallest
@@ -424,16 +438,18 @@ __global__ __launch_bounds__(256) void quantize_mxfp8_kernel(const T* __restrict
 // MXFP8 of bf16 blocks along rows with transposed output (V of the FP8 P/V
 // route), staged like the MXFP4 V^T kernel: a workgroup takes 64 columns x 256
 // rows (32 column pairs x 8 blocks, 4-byte row loads), parks its payloads and
-// scale bytes in LDS and writes each column's 8 blocks as one 256-byte run.
+// scale bytes in LDS and writes each column's 8 blocks as one 256-byte run (each
+// store instruction of a wave covers 64 contiguous bytes of 16 columns) and its
+// 8 scale bytes with one store.
 // cols % 64 == 0; blocks past the last are skipped (their threads still meet
 // the barrier).
 __global__ __launch_bounds__(256) void quantize_mxfp8_bf16_cols_staged_kernel(
     const uint16_t* __restrict__ src, int64_t batch, int64_t rows, int64_t cols, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales) {
-  __shared__ uint4 code_lds[64][8][2];
-  __shared__ uint8_t scale_lds[64][8];
+  __shared__ uint4 code_lds[64][16];  // column x 16-byte chunk of its 256-byte run
+  __shared__ uint2 scale_lds[64];      // 8 bytes per column
   const int64_t nblk = rows / 32, ngrp = (nblk + 7) / 8, ncg = cols / 64;
-  const int64_t grp = blockIdx.x % ngrp, cg = (blockIdx.x / ngrp) % ncg, b = blockIdx.x / (ngrp * ncg);
+  const int64_t cg = blockIdx.x % ncg, grp = (blockIdx.x / ncg) % ngrp, b = blockIdx.x / (ngrp * ncg);
   const int tid = threadIdx.x, cp = tid % 32, lb = tid / 32;
   const int64_t blk = grp * 8 + lb;
   if (blk < nblk) {
@@ -446,30 +462,26 @@ __global__ __launch_bounds__(256) void quantize_mxfp8_bf16_cols_staged_kernel(
       v1[j] = __builtin_bit_cast(float, pr & 0xffff0000u);
     }
     unsigned w[8];
-    scale_lds[2 * cp][lb] = (uint8_t)mxfp8_block(v0, w);
-    code_lds[2 * cp][lb][0] = uint4{w[0], w[1], w[2], w[3]};
-    code_lds[2 * cp][lb][1] = uint4{w[4], w[5], w[6], w[7]};
-    scale_lds[2 * cp + 1][lb] = (uint8_t)mxfp8_block(v1, w);
-    code_lds[2 * cp + 1][lb][0] = uint4{w[0], w[1], w[2], w[3]};
-    code_lds[2 * cp + 1][lb][1] = uint4{w[4], w[5], w[6], w[7]};
+    uint8_t* sb = reinterpret_cast<uint8_t*>(scale_lds);
+    sb[16 * cp + lb] = (uint8_t)mxfp8_block(v0, w);
+    code_lds[2 * cp][2 * lb] = uint4{w[0], w[1], w[2], w[3]};
+    code_lds[2 * cp][2 * lb + 1] = uint4{w[4], w[5], w[6], w[7]};
+    sb[16 * cp + 8 + lb] = (uint8_t)mxfp8_block(v1, w);
+    code_lds[2 * cp + 1][2 * lb] = uint4{w[0], w[1], w[2], w[3]};
+    code_lds[2 * cp + 1][2 * lb + 1] = uint4{w[4], w[5], w[6], w[7]};
   }
   __syncthreads();
-  // thread t writes blocks 2 (t % 4) and 2 (t % 4) + 1 of column t / 4
+  // thread t writes 16-byte chunks (t % 4) + 4 k, k < 4, of column t / 4 (chunk
+  // 2 l + h is half h of block l)
   const int c = tid / 4, part = tid % 4;
   const int64_t col = b * cols + cg * 64 + c;
   uint8_t* cdst = codes + (col * nblk + grp * 8) * 32;
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int l = 2 * part + k;
-    if (grp * 8 + l < nblk) {
-      *reinterpret_cast<uint4*>(cdst + l * 32) = code_lds[c][l][0];
-      *reinterpret_cast<uint4*>(cdst + l * 32 + 16) = code_lds[c][l][1];
-    }
+  for (int k = 0; k < 4; ++k) {
+    const int ch = part + 4 * k;
+    if (grp * 8 + ch / 2 < nblk) *reinterpret_cast<uint4*>(cdst + ch * 16) = code_lds[c][ch];
   }
-  if (tid < 64) {
-    const int64_t colx = b * cols + cg * 64 + tid;
-    for (int l = 0; l < 8 && grp * 8 + l < nblk; ++l) scales[colx * nblk + grp * 8 + l] = scale_lds[tid][l];
-  }
+  if (tid < 64) store_scale_run(scales + (b * cols + cg * 64 + tid) * nblk + grp * 8, scale_lds[tid], nblk, grp);
 }
 
 hipError_t launch_quantize_mxfp4(const void* src, int src_dtype, int64_t batch, int64_t rows, int64_t cols, int axis,

@@ -31,6 +31,17 @@ def test_ragged_random(fa, dtype, axis):
     _check(fa, x, axis)
 
 
+@pytest.mark.parametrize("shape", [(3, 96, 192), (2, 256, 64), (1, 352, 128), (2, 512, 128)])
+def test_staged_bf16_vt(fa, shape):
+    """bf16 V^T with whole 64-column groups takes the staged kernel: ragged last
+    groups of blocks (96 and 352 rows: 3 and 11 blocks per column, scale bytes
+    stored one by one) and whole ones (8-byte scale stores), one to three column
+    groups, values over 40 binades."""
+    g = torch.Generator().manual_seed(shape[1] + 3 * shape[2])
+    x = (torch.randn(*shape, generator=g) * torch.exp2(torch.randint(-20, 20, shape, generator=g))).to(torch.bfloat16)
+    _check(fa, x, -2)
+
+
 @pytest.mark.parametrize("axis", [-1, -2])
 def test_adversarial_blocks(fa, axis):
     blocks = []
@@ -192,7 +203,7 @@ def test_mxfp8_adversarial_blocks(fa, axis):
     _check8(fa, x, axis)
 
 
-@pytest.mark.parametrize("shape", [(3, 96, 192), (2, 256, 64)])
+@pytest.mark.parametrize("shape", [(3, 96, 192), (2, 256, 64), (1, 352, 128), (2, 512, 128)])
 def test_mxfp8_staged_bf16(fa, shape):
     """bf16 V^T with whole 64-column groups takes the staged kernel: a ragged
     last group of blocks (96 rows) and full ones, values over 40 binades."""
