@@ -547,6 +547,11 @@ def _counter_view(c, ms):
     return v
 
 
+def _progress(msg):
+    """One line on stderr per finished stage, so a long run shows where it is."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -625,7 +630,9 @@ def main():
     pair = {"fp4": fp4_step}
     if not args.no_bf16:
         pair["bf16"] = bf16_step
+    _progress(f"timed region: {args.steps} steps, {fp4_ms:.4f} ms per step")
     med, _ = _time_windows(torch, pair, 300.0, args.windows)
+    _progress("interleaved FP4 / BF16 windows done")
     fns = {}
     # native-exponential mixing (k of the 16 pairs of each 32-key block): the
     # `accurate` policy's quarter and the exp2-only route, same inputs
@@ -652,6 +659,7 @@ def main():
     bf16_tflops = flops / (med["bf16"] * 1e-3) / 1e12 if "bf16" in med else None
     c_online = _route_counters("online", name)
     traffic = round(c_online["hbm_bytes"]) if c_online and "hbm_bytes" in c_online else None
+    _progress("route and quantizer windows done")
     clk = measured_clock_ghz(torch, fa, ops, w)
     peak_clk = MXFP4_PEAK_TFLOPS * clk / SPEC_CLOCK_GHZ
     stream_blocks = min(1024, ops[0].numel() // (256 * 64))  # 64 operand bytes per thread
@@ -726,11 +734,14 @@ def main():
     del bf, out16
     if not args.no_other_configs and not args.no_bf16 and args.workload is None:
         line["configs"] = other_configs(torch, fa, name)
+        _progress("other workloads done")
     if not args.no_paper_shapes and not args.no_bf16:
         line["paper_shapes"] = paper_shape_sweep(torch, fa)
+        _progress("paper shapes done")
     if not args.no_cpu_baseline:
         import numpy as np
         line["cpu_baseline"], (rows, o_ref) = cpu_oracle_baseline(w, q_cpu, k_cpu, v_cpu)
+        _progress("oracle baseline done")
         # parity of the timed launch on the rows the oracle computed
         fp4_step()
         torch.cuda.synchronize()
