@@ -19,7 +19,9 @@ def _ptr(t):
 
 
 def _stream(t):
-    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+    # the raw handle of torch's current stream on t's device (the same value as
+    # torch.cuda.current_stream(device).cuda_stream, without building a Stream)
+    return ctypes.c_void_p(torch._C._cuda_getCurrentRawStream(t.get_device()))
 
 
 def _same_device(*tensors):
@@ -33,18 +35,21 @@ def _same_device(*tensors):
 
 
 def _launch(device, fn, *args):
+    if device.index == torch.cuda.current_device():
+        check(fn(*args))
+        return
     with torch.cuda.device(device):
         check(fn(*args))
 
 
 def _need(t, name, dtype=None, ndim=None):
-    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise ValueError(f"{name} must be a GPU tensor")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
         raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
-    if ndim is not None and t.dim() != ndim:
+    if ndim is not None and t.ndim != ndim:
         raise ValueError(f"{name} must have {ndim} dimensions, got shape {tuple(t.shape)}")
 
 
