@@ -1,0 +1,53 @@
+"""Every forward route on shapes chosen at the launch rules' boundaries, against
+the oracle on sampled rows (codes, block exponents, row reference and
+denominator through the test entry point; O and LSE through the forward).
+
+The shapes: exactly one full round of eight-wave workgroups; one workgroup past
+a round and a last round of 64 (both take the four-wave tail launch on the
+plain route, eight waves on the causal and FP8 routes); a last round of 224
+(eight waves); more than five rounds; sequence lengths that are odd multiples
+of 128 (four-wave launch), with batch > 1; the longest sequence below which
+the grid leaves CUs idle; and the smallest problem.  Rows: the first and last
+of the tensor and of a head, and seeded random ones."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from test_gpu_forward import _run_and_check, _run_fp8, _run_guarded
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # B, H, N, d
+    (1, 32, 2048, 128),    # 256 eight-wave workgroups: one full round
+    (1, 257, 256, 128),    # 257: one past a round (tail rule)
+    (5, 64, 256, 128),     # 320: last round 64 (tail rule)
+    (2, 40, 1536, 128),    # 480: last round 224 (eight waves)
+    (1, 1290, 256, 128),   # 1290: six rounds (eight waves)
+    (3, 7, 1664, 128),     # N = 13 x 128: four-wave launch
+    (2, 3, 4224, 64),      # N = 33 x 128, d = 64 (three waves per SIMD)
+    (1, 3, 12288, 128),    # 144 workgroups: fewer than the CUs
+    (1, 6, 8320, 64),      # N = 65 x 128
+    (1, 1, 128, 128),      # one tile
+]
+
+
+def _inputs(B, H, N, d):
+    g = torch.Generator().manual_seed(B * 1000003 + H * 1009 + N * 7 + d)
+    q, k, v = (torch.randn(B, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    host64 = tuple(workloads.as_f64(t) for t in (q, k, v))
+    rows = np.random.default_rng(N + H).integers(0, B * H * N, 40)
+    rows = np.unique(np.concatenate([rows, [0, N - 1, B * H * N - N, B * H * N - 1]]))
+    return host64, (q.cuda(), k.cuda(), v.cuda()), rows
+
+
+@pytest.mark.parametrize("B,H,N,d", SHAPES)
+def test_every_route_at_launch_boundaries(B, H, N, d):
+    import paper_2609_04105_amd as fa
+    host64, dev, rows = _inputs(B, H, N, d)
+    label = f"sweep B{B} H{H} N{N} d{d}"
+    _run_and_check(fa, host64, dev, rows, label)
+    _run_and_check(fa, host64, dev, rows, label + " causal", causal=True, lse=True)
+    _run_and_check(fa, host64, dev, rows, label + " ex2 4", ex2_pairs=4)
+    _run_guarded(fa, host64, dev, rows, label + " guard", 110, 16)
+    _run_fp8(fa, host64, dev, rows, label + " fp8")
