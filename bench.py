@@ -3,6 +3,7 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --profile-run                  (one launch per route, for rocprofv3 passes)
     python bench.py --counter-summary P0 P1 P2 P3  (writes profiles/counters_routes.json)
+    python bench.py --power-run                    (board power, clocks and the stream's occupancy sweep)
 
 A step is one forward pass (QK on scaled FP4 matrix cores, Direct-P, PV, the
 epilogue) over the whole workload with MXFP4 operands already resident in HBM;
@@ -16,7 +17,7 @@ inputs (windows interleaved with the FP4 ones, the paper's speedup
 t_BF16 / t_FP4), the roofline of the forward kernel against the dense MXFP4
 matrix peak (and, beside it, the shader clock the kernel ran at and the rate
 a stream of FP4 matrix products alone sustains on the workload's K and Q
-codes), HBM traffic and hardware-counter figures per route from the committed
+codes, two waves per SIMD), the quantizer's HBM roofline, HBM traffic and hardware-counter figures per route from the committed
 counter file (only while it matches the kernel sources), the other routes
 (native-exponential pairs, the sampled guard, FP8 P/V, causal with LSE), the
 other four workloads, both kernels on the shapes the paper reports (D128 and
@@ -336,7 +337,16 @@ def measured_clock_ghz(torch, fa, ops, w, launches=5):
     return cyc / (ticks / 100e6) / 1e9
 
 
-def sustained_mfma_tflops(torch, fa, a_codes, b_codes, blocks=1024, iters=100000, launches=7):
+def stream_blocks(torch):
+    """Workgroups of the matrix-product stream: two per CU (four-wave workgroups,
+    so two waves per SIMD, all resident in one round).  The stream's rate falls
+    with three or more waves per SIMD (on zero bytes 9.7 PFLOP/s at two, 7.0 at
+    three, 6.3 when four are asked for and three fit), so this is the launch
+    that shows the matrix unit's ceiling."""
+    return 2 * torch.cuda.get_device_properties(torch.cuda.current_device()).multi_processor_count
+
+
+def sustained_mfma_tflops(torch, fa, a_codes, b_codes, blocks=512, iters=200000, launches=7):
     """Rate of a stream of FP4 32x32x64 matrix products with nothing else running,
     on operand bytes of the workload (the QK product's K and Q codes): the matrix
     unit's sustained ceiling on this board for this data, beside the spec peak.
@@ -547,6 +557,179 @@ def _counter_view(c, ms):
     return v
 
 
+_SMI_SAMPLER = r"""
+import json, os, subprocess, sys, time
+parent = os.getppid()
+with open(sys.argv[1], "a") as f:
+    while os.getppid() == parent:   # ends with the process that started it
+        t = time.time()
+        try:
+            r = subprocess.run(["amd-smi", "metric", "--power", "--clock", "--temperature", "--json"],
+                               capture_output=True, text=True, timeout=30)
+            out = r.stdout
+        except Exception as e:
+            out = json.dumps({"error": str(e)[:200]})
+        f.write(json.dumps({"t": t, "out": out}) + "\n")
+        f.flush()
+        time.sleep(0.2)
+"""
+
+
+def start_power_sampler(path):
+    """Start the amd-smi sampler as a child process (before this process makes
+    any HIP call): every ~0.2 s it appends a timestamped reading of every card
+    to ``path``.  amd-smi is only read: power, clocks, temperature."""
+    import subprocess
+    return subprocess.Popen([sys.executable, "-c", _SMI_SAMPLER, path], stdout=subprocess.DEVNULL,
+                            stderr=subprocess.DEVNULL)
+
+
+def _smi_cards(text):
+    """Per card of one amd-smi JSON reading: socket power (W), the shader clock of
+    each XCD (MHz) and the hotspot temperature (C); None where not reported."""
+    data = json.loads(text)
+    cards = data["gpu_data"] if isinstance(data, dict) else data
+    res = []
+    for g in cards:
+        def val(x):
+            return x.get("value") if isinstance(x, dict) else None
+        clocks = [val(c.get("clk", {})) for key, c in g.get("clock", {}).items() if key.startswith("gfx_")]
+        res.append({"gpu": g.get("gpu"), "power_w": val(g.get("power", {}).get("socket_power")),
+                    "gfx_mhz": [c for c in clocks if c is not None],
+                    "hotspot_c": val(g.get("temperature", {}).get("hotspot"))})
+    return res
+
+
+def power_run(torch, fa, sampler, sample_path, seconds=4.0):
+    """Board power, shader clocks and hotspot temperature (amd-smi readings taken
+    by ``sampler``) while each load runs back to back for about ``seconds``: the
+    card idle; the FP4 matrix-product stream (four independent 32x32x64 products
+    per thread, nothing else) on zero bytes, on a constant byte (every code 1.0),
+    on random bytes and on the long workload's K and Q codes; the MXFP4 forward and the BF16 kernel on
+    the long workload.  Then the stream's rate at one to four workgroups per CU.
+    Prints one JSON line: per load the delivered TFLOP/s and the medians of the
+    readings, taken while it ran, of the card whose power rose the most under the
+    forward, and the stream's rate per occupancy."""
+    import workloads
+    w = workloads.WORKLOADS[workloads.BENCH_WORKLOAD]
+    q, k, v = (t.cuda() for t in workloads.generate(w))
+    ops = fa.quantize_qkv(q, k, v)
+    bf = tuple(t.to(torch.bfloat16) for t in (q, k, v))
+    out = torch.empty((w.B, w.H, w.N, w.d), dtype=torch.float32, device="cuda")
+    blocks, iters = stream_blocks(torch), 200000
+    nbytes = blocks * 256 * 64
+    stream_flop = blocks * 4 * iters * 4 * 2.0 * 32 * 32 * 64
+    g = torch.Generator(device="cuda").manual_seed(5)
+    operands = {
+        "zero": (torch.zeros((nbytes,), dtype=torch.uint8, device="cuda"),) * 2,
+        "constant": (torch.full((nbytes,), 0x22, dtype=torch.uint8, device="cuda"),) * 2,
+        "random": tuple(torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device="cuda", generator=g)
+                        for _ in range(2)),
+        "workload": (ops[2].reshape(-1)[:nbytes], ops[0].reshape(-1)[:nbytes]),
+    }
+    loads = [("idle", None, 0.0)]
+    for kind, (a, b) in operands.items():
+        loads.append((f"mfma_stream_{kind}", lambda a=a, b=b: fa.debug_mfma_stream(a, b, blocks, iters), stream_flop))
+    loads.append(("mxfp4_forward", lambda: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out), w.flops))
+    loads.append(("bf16_forward", lambda: fa.forward_bf16(*bf, softmax_scale=w.softmax_scale, out=out), w.flops))
+
+    results = []
+    for name, fn, flop in loads:
+        if fn is not None:
+            fn()
+        torch.cuda.synchronize()
+        calls = 0
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        t0 = time.time()
+        while time.time() - t0 < seconds:
+            if fn is None:
+                time.sleep(0.05)
+                continue
+            fn()
+            calls += 1
+            if calls % 8 == 0:
+                torch.cuda.synchronize()
+        end.record()
+        torch.cuda.synchronize()
+        t1 = time.time()
+        ms = start.elapsed_time(end)
+        results.append({"load": name, "calls": calls, "window": (t0, t1),
+                        "tflops": round(flop * calls / (ms * 1e-3) / 1e12, 1) if calls else None})
+        _progress(f"power run: {name} done")
+    clk = measured_clock_ghz(torch, fa, ops, w)
+    # the stream's rate against its occupancy: one to three waves per SIMD, and
+    # four asked for where three fit (a second, lone round), ~1.5 s each
+    occupancy = []
+    cus = torch.cuda.get_device_properties(torch.cuda.current_device()).multi_processor_count
+    for kind in ("zero", "random"):
+        a, b = operands[kind]
+        for per_cu, label in ((1, "1 wave per SIMD"), (2, "2 waves per SIMD"), (3, "3 waves per SIMD"),
+                              (4, "4 asked, 3 fit")):
+            nb = per_cu * cus
+            big = torch.cat([a] * per_cu) if per_cu > 1 else a
+            it = iters * 2 // per_cu
+            fa.debug_mfma_stream(big, big, nb, 1000)
+            torch.cuda.synchronize()
+            calls, flop_total = 0, 0.0
+            start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            start.record()
+            t0 = time.time()
+            while time.time() - t0 < 1.5:
+                _, f = fa.debug_mfma_stream(big, big, nb, it)
+                calls += 1
+                flop_total += f
+                if calls % 4 == 0:
+                    torch.cuda.synchronize()
+            end.record()
+            torch.cuda.synchronize()
+            occupancy.append({"operands": kind, "workgroups": nb, "occupancy": label,
+                              "tflops": round(flop_total / (start.elapsed_time(end) * 1e-3) / 1e12, 1)})
+            del big
+    _progress("power run: stream occupancy sweep done")
+    time.sleep(0.5)
+    sampler.terminate()
+    sampler.wait(timeout=30)
+    readings = []
+    with open(sample_path) as f:
+        for line in f:
+            rec = json.loads(line)
+            try:
+                readings.append((rec["t"], _smi_cards(rec["out"])))
+            except (ValueError, KeyError, TypeError):
+                pass
+
+    def med(xs):
+        xs = sorted(x for x in xs if x is not None)
+        return xs[len(xs) // 2] if xs else None
+
+    def during(r, i, key):
+        # readings started well inside the load's window (the tool takes a while)
+        t0, t1 = r["window"]
+        return [cards[i].get(key) for t, cards in readings if t0 + 0.5 <= t <= t1 - 0.5 and len(cards) > i]
+
+    n_cards = max((len(c) for _, c in readings), default=0)
+    fwd = next(r for r in results if r["load"] == "mxfp4_forward")
+    idle = results[0]
+    rise = [(med(during(fwd, i, "power_w")) or 0) - (med(during(idle, i, "power_w")) or 0) for i in range(n_cards)]
+    card = max(range(n_cards), key=lambda i: rise[i]) if n_cards else None
+    for r in results:
+        if card is not None:
+            pw = during(r, card, "power_w")
+            clocks = [c for cs in during(r, card, "gfx_mhz") if cs for c in cs]
+            hs = [x for x in during(r, card, "hotspot_c") if x is not None]
+            r.update({"samples": len(pw), "socket_power_w_median": med(pw),
+                      "socket_power_w_max": max((x for x in pw if x is not None), default=None),
+                      "gfx_clock_mhz_median": med(clocks),
+                      "gfx_clock_mhz_range": [min(clocks), max(clocks)] if clocks else None,
+                      "hotspot_c_max": max(hs) if hs else None})
+        del r["window"]
+    print(json.dumps({"power_run": results, "stream_occupancy": occupancy, "card_index_in_tool": card,
+                      "n_cards_listed": n_cards,
+                      "forward_in_kernel_clock_ghz": round(clk, 3), "workload": w.name,
+                      "load_seconds": seconds}), flush=True)
+
+
 def _progress(msg):
     """One line on stderr per finished stage, so a long run shows where it is."""
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -567,6 +750,9 @@ def main():
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3 passes: one 256 MiB device copy (traffic calibration), then one launch "
                          "of every profiled route; prints no JSON")
+    ap.add_argument("--power-run", action="store_true",
+                    help="board power, clocks and hotspot temperature (amd-smi) while the matrix-product stream, "
+                         "the MXFP4 forward and the BF16 kernel each run back to back; one JSON line")
     ap.add_argument("--counter-summary", nargs="+", metavar="CSV",
                     help="write the per-route counter file from the --profile-run counter CSVs, one per pass "
                          "in the order of PASSES (no GPU use)")
@@ -579,6 +765,11 @@ def main():
               "and nothing here uses a second GPU; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    sampler = None
+    if args.power_run:   # started before this process touches the GPU
+        import tempfile
+        sample_path = os.path.join(tempfile.mkdtemp(prefix="fp4attn_power_"), "smi.jsonl")
+        sampler = start_power_sampler(sample_path)
     import torch
     import workloads
     import paper_2609_04105_amd as fa
@@ -587,6 +778,14 @@ def main():
     torch.cuda.set_device(dev)
     if args.profile_run:
         profile_run(torch, fa)
+        return
+    if args.power_run:
+        try:
+            power_run(torch, fa, sampler, sample_path)
+        finally:
+            if sampler.poll() is None:
+                sampler.terminate()
+                sampler.wait(timeout=30)
         return
 
     name = args.workload or workloads.BENCH_WORKLOAD
@@ -662,9 +861,9 @@ def main():
     _progress("route and quantizer windows done")
     clk = measured_clock_ghz(torch, fa, ops, w)
     peak_clk = MXFP4_PEAK_TFLOPS * clk / SPEC_CLOCK_GHZ
-    stream_blocks = min(1024, ops[0].numel() // (256 * 64))  # 64 operand bytes per thread
-    stream = sustained_mfma_tflops(torch, fa, ops[2].reshape(-1), ops[0].reshape(-1), blocks=stream_blocks) \
-        if stream_blocks >= 1 else None
+    n_stream = min(stream_blocks(torch), ops[0].numel() // (256 * 64))  # 64 operand bytes per thread
+    stream = sustained_mfma_tflops(torch, fa, ops[2].reshape(-1), ops[0].reshape(-1), blocks=n_stream) \
+        if n_stream >= 1 else None
     roof = {
         "bound": "mfma",
         "achieved": round(tflops, 2),
