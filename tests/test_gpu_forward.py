@@ -193,16 +193,17 @@ def _check_byte_operands(fa, ops_cpu, rows, label, causal=False, guard=None, pv_
     check_output(got, ref["O"], label)
 
 
-@pytest.mark.parametrize("causal", [False, True])
-def test_longest_sequence_sampled_rows(fa, causal):
+@pytest.mark.parametrize("d,causal", [(128, False), (128, True), (64, False), (64, True)])
+def test_longest_sequence_sampled_rows(fa, d, causal):
     """N = 2^22 keys, the largest the entry point accepts: every byte offset within
-    the head near its 32-bit limit, 32768 key tiles per workgroup.  Rows: the first
-    and last of the sequence, of a query tile and of a workgroup, and random ones."""
+    the head near its 32-bit limit, 32768 key tiles per workgroup; d = 64 takes
+    128-query workgroups at three waves per SIMD.  Rows: the first and last of the
+    sequence, of a query tile and of a workgroup, and random ones."""
     N = 1 << 22
-    ops_cpu = workloads.random_mxfp4_operands(1, 1, N, 128, seed=22)
-    rows = np.unique(np.concatenate([[0, 1, 255, 256, N // 2 + 31, N - 257, N - 256, N - 1],
-                                     np.random.default_rng(22).integers(0, N, 8)]))
-    _check_byte_operands(fa, ops_cpu, rows, f"N=2^22 causal={causal}", causal=causal)
+    ops_cpu = workloads.random_mxfp4_operands(1, 1, N, d, seed=22 + d)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, 255, 256, N // 2 + 31, N - 257, N - 256, N - 129, N - 128,
+                                      N - 1], np.random.default_rng(22).integers(0, N, 8)]))
+    _check_byte_operands(fa, ops_cpu, rows, f"N=2^22 d{d} causal={causal}", causal=causal)
 
 
 @pytest.mark.parametrize("route", ["guard_110_16", "fp8_pv"])
