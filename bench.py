@@ -830,7 +830,7 @@ def main():
     if not args.no_bf16:
         pair["bf16"] = bf16_step
     _progress(f"timed region: {args.steps} steps, {fp4_ms:.4f} ms per step")
-    med, _ = _time_windows(torch, pair, 300.0, args.windows)
+    med, windows = _time_windows(torch, pair, 300.0, args.windows)
     _progress("interleaved FP4 / BF16 windows done")
     fns = {}
     # native-exponential mixing (k of the 16 pairs of each 32-key block): the
@@ -910,6 +910,9 @@ def main():
         "bf16_pct_peak": None if bf16_tflops is None else round(100 * bf16_tflops / BF16_PEAK_TFLOPS, 2),
         "speedup_vs_bf16": None if "bf16" not in med else round(med["bf16"] / med["fp4"], 3),
         "fp4_ms_median_interleaved": round(med["fp4"], 5),
+        "fp4_ms_min_interleaved": round(min(windows["fp4"]), 5),
+        "bf16_ms_min_interleaved": None if "bf16" not in windows else round(min(windows["bf16"]), 5),
+        "interleaved_windows": args.windows,
         "bf16_ms_median_interleaved": None if "bf16" not in med else round(med["bf16"], 5),
         "quantize_qkv_ms": round(qms["quant"], 5),
         "quantizer": quantizer,
