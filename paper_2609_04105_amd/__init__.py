@@ -15,6 +15,7 @@ from ._lib import (  # noqa: F401
     lib,
 )
 from .api import (  # noqa: F401
+    attention_mxfp4,
     debug_directp_mxfp4,
     debug_mfma_stream,
     forward_bf16,

@@ -193,6 +193,17 @@ def forward_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, sof
     return out
 
 
+def attention_mxfp4(q, k, v, softmax_scale=None, causal=False, lse=None, ex2_pairs=None, guard=None,
+                    pv_fp8=False, out=None, out_dtype=torch.float32):
+    """Quantize ``q``, ``k``, ``v`` ([B, H, N, d], bf16 or fp32) and run the Direct-P
+    forward in one call: MXFP4 Q and K; V in MXFP4 or, with ``pv_fp8``, MXFP8; K and
+    V in anchor order when ``guard`` is given.  The quantized operands are not kept
+    (use :func:`quantize_qkv` and :func:`forward_mxfp4` to reuse them)."""
+    ops = quantize_qkv(q, k, v, anchored=guard is not None, pv_fp8=pv_fp8)
+    return forward_mxfp4(*ops, softmax_scale=softmax_scale, out=out, out_dtype=out_dtype, ex2_pairs=ex2_pairs,
+                         guard=guard, causal=causal, lse=lse, pv_fp8=pv_fp8)
+
+
 def debug_directp_mxfp4(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, row_ids, softmax_scale=None,
                         affine_a=1.5, affine_b=1.2, out_dtype=torch.float32, wg_clock=False, ex2_pairs=0,
                         guard=None, causal=False, lse=False, pv_fp8=False):

@@ -739,3 +739,16 @@ def test_non_finite_input_propagation(fa, where):
     check_output(got[rows][:, cols], ref["O"][:, cols], f"non-finite {where}, finite entries")
     if where == "v_column":
         check_output(got[:N], ref["O"][:N], "non-finite v_column, head 0 all columns")
+
+
+def test_one_call_attention_equals_two_steps(fa):
+    """attention_mxfp4 (quantize and forward in one call) gives the same bytes as
+    quantize_qkv followed by forward_mxfp4, on every route."""
+    g = torch.Generator().manual_seed(31)
+    q, k, v = (torch.randn(1, 2, 512, 64, generator=g).to(torch.bfloat16).cuda() for _ in range(3))
+    for opts in ({}, {"causal": True}, {"ex2_pairs": 4}, {"guard": (110, 16)}, {"pv_fp8": True}):
+        one = fa.attention_mxfp4(q, k, v, **opts)
+        ops = fa.quantize_qkv(q, k, v, anchored="guard" in opts, pv_fp8=opts.get("pv_fp8", False))
+        two = fa.forward_mxfp4(*ops, **opts)
+        torch.cuda.synchronize()
+        assert torch.equal(one, two), opts
