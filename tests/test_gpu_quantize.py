@@ -238,3 +238,34 @@ def test_mxfp8_workload_v(fa):
     cg, sg = fa.quantize_mxfp8(v.cuda(), axis=-2)
     co, so = fp8pv.quantize(workloads.as_f64(v), axis=-2)
     assert np.array_equal(sg.cpu().numpy(), so) and np.array_equal(cg.cpu().numpy(), co)
+
+
+# (batch, rows, cols): both extents multiples of 32; cols a multiple of 64 or not
+# (the staged V^T kernel or the per-thread one), groups of eight V^T blocks whole
+# or ragged, one to three 64-column groups, single rows and single blocks
+SWEEP_SHAPES = [(1, 32, 32), (1, 32, 64), (2, 64, 96), (3, 96, 128), (1, 160, 192), (2, 224, 64), (1, 256, 160),
+                (4, 288, 128), (1, 512, 32), (2, 800, 64), (1, 1056, 128), (3, 32, 320)]
+
+
+@pytest.mark.parametrize("shape", SWEEP_SHAPES)
+def test_quantizer_shape_sweep(fa, shape):
+    """MXFP4 (both axes, bf16 and fp32 inputs) and MXFP8 (bf16 and fp32) against the
+    oracle, bit for bit, over values spanning 24 binades with a few zero and tiny
+    blocks; with rows a multiple of 128 also the anchored form."""
+    from oracle import fp8pv, guard
+    B, R, C = shape
+    g = torch.Generator().manual_seed(B * 1009 + R * 31 + C)
+    x = torch.randn(B, R, C, generator=g) * torch.exp2(torch.randint(-12, 12, (B, R, C), generator=g).float())
+    x[:, :, :32] *= (torch.rand(B, R, 1, generator=g) > 0.1).float()      # some zero blocks along a row
+    x[:, 0, :] *= 2.0 ** -120                                             # a row of tiny values
+    for dtype in (torch.bfloat16, torch.float32):
+        xd = x.to(dtype)
+        for axis in (-1, -2):
+            _check(fa, xd, axis)
+            _check8(fa, xd, axis)
+        if R % 128 == 0:
+            perm = guard.anchor_permutation(R)
+            for axis in (-1, -2):
+                cg, sg = fa.quantize_mxfp4(xd.cuda(), axis=axis, n_anchor=128)
+                co, so = mxfp4.quantize(workloads.as_f64(xd)[:, perm], axis=axis)
+                assert np.array_equal(sg.cpu().numpy(), so) and np.array_equal(cg.cpu().numpy(), co), (dtype, axis)
