@@ -132,3 +132,34 @@ def test_bf16_longest_sequence_sampled_rows(fa):
     worst = float(row_rel_l2(got, ref).max())
     print(f"[bf16 N=2^22] rel-L2 {rel:.3e} cos {cos:.8f} worst row rel-L2 {worst:.3e}", flush=True)
     assert rel <= REL_MAX and cos >= COS_MIN and worst <= ROW_REL_MAX, (rel, cos, worst)
+
+
+@pytest.mark.parametrize("B,H,N,d", [(1, 32, 2048, 128), (1, 31, 2048, 128), (1, 16, 2048, 64), (1, 15, 2048, 64),
+                                     (3, 7, 1664, 128), (2, 5, 640, 64), (1, 1290, 256, 128), (1, 1, 128, 128)])
+def test_bf16_launch_boundaries(fa, B, H, N, d):
+    """Both sides of the launch rule (eight-wave workgroups from 256 of them at
+    d = 128 and from 128 at d = 64, four-wave below and when N is not a multiple
+    of 256), many heads, one tile; 40 seeded rows plus the first and last of the
+    tensor and of a head."""
+    g = torch.Generator().manual_seed(B * 1000003 + H * 1009 + N * 7 + d)
+    q, k, v = (torch.randn(B, H, N, d, generator=g).to(torch.bfloat16) for _ in range(3))
+    rows = np.random.default_rng(N + H).integers(0, B * H * N, 40)
+    rows = np.unique(np.concatenate([rows, [0, N - 1, B * H * N - N, B * H * N - 1]]))
+    heads = np.unique(rows // N)
+    sel = torch.from_numpy(heads)
+    # only the heads the rows touch go to the exact reference
+    host64 = tuple(workloads.as_f64(t.reshape(B * H, 1, N, d)[sel].reshape(1, len(heads), N, d)) for t in (q, k, v))
+    local = np.searchsorted(heads, rows // N) * N + rows % N
+    s = 1.0 / np.sqrt(d)
+    print(f"[bf16 sweep B{B} H{H} N{N} d{d}] rows={len(rows)}", flush=True)
+    out = fa.forward_bf16(q.cuda(), k.cuda(), v.cuda())
+    torch.cuda.synchronize()
+    got = out.reshape(-1, d)[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    ref = np.zeros((len(rows), d))
+    for i, bh in enumerate(heads):
+        idx = np.nonzero(rows // N == bh)[0]
+        ref[idx] = exact.attention(host64[0][0, i][local[idx] % N], host64[1][0, i], host64[2][0, i], s)
+    rel, cos = rel_l2_cos(got, ref)
+    worst = float(row_rel_l2(got, ref).max())
+    print(f"[bf16 sweep B{B} H{H} N{N} d{d}] rel-L2 {rel:.3e} cos {cos:.8f} worst row {worst:.3e}", flush=True)
+    assert rel <= REL_MAX and cos >= COS_MIN and worst <= ROW_REL_MAX, (rel, cos, worst)
