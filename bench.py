@@ -600,6 +600,44 @@ def _smi_cards(text):
     return res
 
 
+def _stop_sampler(sampler):
+    if sampler.poll() is None:
+        sampler.terminate()
+        sampler.wait(timeout=30)
+
+
+def board_readings(path, t0, t1):
+    """Medians of the amd-smi readings taken inside [t0, t1] (wall clock) of the
+    card whose power is highest there: socket power, XCD shader clocks, hotspot
+    temperature.  None if the window holds no reading."""
+    cards_by_time = []
+    try:
+        with open(path) as f:
+            for line in f:
+                try:
+                    rec = json.loads(line)
+                    if t0 <= rec["t"] <= t1:
+                        cards_by_time.append(_smi_cards(rec["out"]))
+                except (ValueError, KeyError, TypeError):
+                    continue   # a line still being written, or a failed reading
+    except OSError:
+        return None
+    if not cards_by_time:
+        return None
+
+    def med(xs):
+        xs = sorted(x for x in xs if x is not None)
+        return xs[len(xs) // 2] if xs else None
+    n = max(len(c) for c in cards_by_time)
+    card = max(range(n), key=lambda i: med([c[i]["power_w"] for c in cards_by_time if len(c) > i]) or 0)
+    rows = [c[card] for c in cards_by_time if len(c) > card]
+    clocks = [x for r in rows for x in r["gfx_mhz"]]
+    return {"samples": len(rows), "socket_power_w_median": med([r["power_w"] for r in rows]),
+            "gfx_clock_mhz_median": med(clocks), "hotspot_c_max": max((r["hotspot_c"] for r in rows
+                                                                      if r["hotspot_c"] is not None), default=None),
+            "source": "amd-smi metric (read-only), sampled during the timed region"}
+
+
 def power_run(torch, fa, sampler, sample_path, seconds=4.0):
     """Board power, shader clocks and hotspot temperature (amd-smi readings taken
     by ``sampler``) while each load runs back to back for about ``seconds``: the
@@ -750,6 +788,8 @@ def main():
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3 passes: one 256 MiB device copy (traffic calibration), then one launch "
                          "of every profiled route; prints no JSON")
+    ap.add_argument("--no-board", action="store_true",
+                    help="do not sample board power and clocks (amd-smi) during the timed region")
     ap.add_argument("--power-run", action="store_true",
                     help="board power, clocks and hotspot temperature (amd-smi) while the matrix-product stream, "
                          "the MXFP4 forward and the BF16 kernel each run back to back; one JSON line")
@@ -766,10 +806,16 @@ def main():
         sys.exit(2)
 
     sampler = None
-    if args.power_run:   # started before this process touches the GPU
+    sample_path = None
+    # the board-power sampler is a child process started before this process
+    # touches the GPU; the default run records its readings over the timed region
+    import shutil
+    if args.power_run or (not args.profile_run and not args.no_board and shutil.which("amd-smi")):
+        import atexit
         import tempfile
         sample_path = os.path.join(tempfile.mkdtemp(prefix="fp4attn_power_"), "smi.jsonl")
         sampler = start_power_sampler(sample_path)
+        atexit.register(_stop_sampler, sampler)
     import torch
     import workloads
     import paper_2609_04105_amd as fa
@@ -783,9 +829,7 @@ def main():
         try:
             power_run(torch, fa, sampler, sample_path)
         finally:
-            if sampler.poll() is None:
-                sampler.terminate()
-                sampler.wait(timeout=30)
+            _stop_sampler(sampler)
         return
 
     name = args.workload or workloads.BENCH_WORKLOAD
@@ -816,6 +860,7 @@ def main():
     # the timed region: exactly `steps` forward steps, synchronized on both sides
     torch.cuda.synchronize()
     t_start = time.perf_counter()
+    t_wall0 = time.time()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ev0.record()
     for _ in range(args.steps):
@@ -823,6 +868,7 @@ def main():
     ev1.record()
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_start) * 1e3
+    t_wall1 = time.time()
     fp4_ms = ev0.elapsed_time(ev1) / args.steps
 
     # the paper's speedup convention: FP4 and BF16 windows interleaved
@@ -927,6 +973,7 @@ def main():
         "causal_with_lse": route("causal_lse", med["causal"], causal_flops, flops="4 d B H N (N + 1) / 2"),
         "bf16_counters": None if "bf16" not in med else _counter_view(_route_counters("bf16", name), med["bf16"]),
         "wall_ms_timed_region": round(wall_ms, 3),
+        "board": None if sample_path is None else board_readings(sample_path, t_wall0 + 0.2, t_wall1 - 0.2),
         "roofline": roof,
         "gpu": torch.cuda.get_device_name(dev),
         "gfx_target": torch.cuda.get_device_properties(dev).gcnArchName,
