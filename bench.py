@@ -15,14 +15,16 @@ ops count 4 B H N^2 d per step (eq. hao-flops) over the step time.
 Prints one JSON line.  Also reported: the same-design BF16 kernel on the same
 inputs (windows interleaved with the FP4 ones, the paper's speedup
 t_BF16 / t_FP4), the roofline of the forward kernel against the dense MXFP4
-matrix peak (and, beside it, the shader clock the kernel ran at and the rate
-a stream of FP4 matrix products alone sustains on the workload's K and Q
-codes, two waves per SIMD), the quantizer's HBM roofline, HBM traffic and hardware-counter figures per route from the committed
+matrix peak (and, beside it, the shader clock the kernel holds when run back
+to back, its rate and cycles per workgroup on the workload's codes and on
+all-zero codes, and the rate a stream of FP4 matrix products alone sustains on
+the workload's K and Q codes, two waves per SIMD), the quantizer's HBM
+roofline, HBM traffic and hardware-counter figures per route from the committed
 counter file (only while it matches the kernel sources), the other routes
 (native-exponential pairs, the sampled guard, FP8 P/V, causal with LSE), the
 other four workloads, both kernels on the shapes the paper reports (D128 and
-D64) next to the paper's printed rates, and the CPU oracle timed on the
-workload's sampled rows.  The defaults follow the paper's timing protocol (Sec.
+D64) next to the paper's printed rates, and the CPU oracle timed on a seeded
+sample of the workload's rows.  The defaults follow the paper's timing protocol (Sec.
 "Operator benchmark suites"): 240 warmup steps (over 300 ms), 2200 timed steps
 (about 3 s), and ten interleaved 300 ms windows of each of the FP4 and BF16
 kernels.
@@ -322,19 +324,54 @@ def _time_windows(torch, fns, window_ms, windows):
     return {k: sorted(v)[len(v) // 2] for k, v in res.items()}, res
 
 
-def measured_clock_ghz(torch, fa, ops, w, launches=5):
-    """Shader clock achieved by the timed forward kernel: launched through the
-    test entry point with no rows to dump (the plain forward kernel), each
-    workgroup records the shader-clock cycles and 100 MHz constant-clock ticks
-    of its residency; the ratio of the sums over workgroups and launches."""
+def _sustained_clock(torch, fa, ops, w, out, seconds):
+    """Run the timed forward back to back for ``seconds`` on the operands ``ops``;
+    over the second half, launches with the workgroup clock record give the
+    kernel's shader clock and the median shader cycles per workgroup.  Returns
+    (TFLOP/s over every launch of the window, clock in GHz, cycles per workgroup)."""
     no_rows = torch.zeros(0, dtype=torch.int64, device=ops[0].device)
-    cyc = ticks = 0
-    for _ in range(launches):
-        r = fa.debug_directp_mxfp4(*ops, no_rows, softmax_scale=w.softmax_scale, wg_clock=True)
-        c = r["wg_clock"].cpu()
-        cyc += int(c[:, 0].sum())
-        ticks += int(c[:, 1].sum())
-    return cyc / (ticks / 100e6) / 1e9
+    fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    t0, n, recs = time.time(), 0, []
+    while time.time() - t0 < seconds:
+        for _ in range(8):
+            fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out)
+        n += 8
+        if time.time() - t0 > seconds / 2:
+            # the record stays on the device until the window ends
+            recs.append(fa.debug_directp_mxfp4(*ops, no_rows, softmax_scale=w.softmax_scale,
+                                               wg_clock=True)["wg_clock"])
+            n += 1
+        torch.cuda.synchronize()
+    e.record()
+    torch.cuda.synchronize()
+    c = torch.cat([r.cpu() for r in recs]).double()
+    c = c[c[:, 0] > 0]   # rows past the launch's workgroup count stay zero
+    return (w.flops * n / (s.elapsed_time(e) * 1e-3) / 1e12, float(c[:, 0].sum() / (c[:, 1].sum() / 100e6) / 1e9),
+            float(c[:, 0].median()))
+
+
+def clock_vs_data(torch, fa, ops, w, out, seconds=1.5):
+    """The timed kernel on the workload's codes and on all-zero Q, K and V^T codes
+    (the same scales, instructions, copies and LDS reads; the products see no data
+    activity), one sustained window each: how much of the gap to the spec peak is
+    the schedule (cycles per workgroup) and how much the clock the chip holds on
+    the data."""
+    zero = list(ops)
+    for i in (0, 2, 4):
+        zero[i] = torch.zeros_like(ops[i])
+    res = {}
+    for label, o in (("workload_codes", ops), ("zero_codes", tuple(zero))):
+        tf, clk, cyc = _sustained_clock(torch, fa, o, w, out, seconds)
+        res[label] = {"tflops": round(tf, 1), "frac_of_peak": round(tf / MXFP4_PEAK_TFLOPS, 4),
+                      "kernel_clock_ghz": round(clk, 3), "cycles_per_workgroup": round(cyc)}
+    for r in res.values():
+        # the rate against the spec peak scaled to the clock the kernel ran at
+        r["frac_at_kernel_clock"] = round(r["tflops"] / (MXFP4_PEAK_TFLOPS * r["kernel_clock_ghz"] / SPEC_CLOCK_GHZ), 4)
+    res["seconds_each"] = seconds
+    return res
 
 
 def stream_blocks(torch):
@@ -661,8 +698,9 @@ def power_run(torch, fa, sampler, sample_path, seconds=4.0):
     by ``sampler``) while each load runs back to back for about ``seconds``: the
     card idle; the FP4 matrix-product stream (four independent 32x32x64 products
     per thread, nothing else) on zero bytes, on a constant byte (every code 1.0),
-    on random bytes and on the long workload's K and Q codes; the MXFP4 forward and the BF16 kernel on
-    the long workload.  Then the stream's rate at one to four workgroups per CU.
+    on random bytes and on the long workload's K and Q codes; the MXFP4 forward on the long workload's
+    codes and on all-zero codes (the same instructions, copies and LDS reads); the BF16 kernel on the
+    long workload.  Then the stream's rate at one to four workgroups per CU.
     Prints one JSON line: per load the delivered TFLOP/s and the medians of the
     readings, taken while it ran, of the card whose power rose the most under the
     forward, and the stream's rate per occupancy."""
@@ -687,6 +725,11 @@ def power_run(torch, fa, sampler, sample_path, seconds=4.0):
     for kind, (a, b) in operands.items():
         loads.append((f"mfma_stream_{kind}", lambda a=a, b=b: fa.debug_mfma_stream(a, b, blocks, iters), stream_flop))
     loads.append(("mxfp4_forward", lambda: fa.forward_mxfp4(*ops, softmax_scale=w.softmax_scale, out=out), w.flops))
+    zero_ops = list(ops)
+    for i in (0, 2, 4):
+        zero_ops[i] = torch.zeros_like(ops[i])
+    loads.append(("mxfp4_forward_zero_codes",
+                  lambda: fa.forward_mxfp4(*zero_ops, softmax_scale=w.softmax_scale, out=out), w.flops))
     loads.append(("bf16_forward", lambda: fa.forward_bf16(*bf, softmax_scale=w.softmax_scale, out=out), w.flops))
 
     results = []
@@ -713,7 +756,7 @@ def power_run(torch, fa, sampler, sample_path, seconds=4.0):
         results.append({"load": name, "calls": calls, "window": (t0, t1),
                         "tflops": round(flop * calls / (ms * 1e-3) / 1e12, 1) if calls else None})
         _progress(f"power run: {name} done")
-    clk = measured_clock_ghz(torch, fa, ops, w)
+    _, clk, _ = _sustained_clock(torch, fa, ops, w, out, 1.5)
     # the stream's rate against its occupancy: one to three waves per SIMD, and
     # four asked for where three fit (a second, lone round), ~1.5 s each
     occupancy = []
@@ -806,6 +849,9 @@ def main():
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3 passes: one 256 MiB device copy (traffic calibration), then one launch "
                          "of every profiled route; prints no JSON")
+    ap.add_argument("--no-clock-vs-data", action="store_true",
+                    help="skip the sustained windows of the timed kernel on the workload's and on zero codes (a "
+                         "traced run keeps the timed kernel's dispatches to the workload's codes)")
     ap.add_argument("--no-board", action="store_true",
                     help="do not sample board power and clocks (amd-smi) during the timed region")
     ap.add_argument("--power-run", action="store_true",
@@ -923,8 +969,11 @@ def main():
     c_online = _route_counters("online", name)
     traffic = round(c_online["hbm_bytes"]) if c_online and "hbm_bytes" in c_online else None
     _progress("route and quantizer windows done")
-    clk = measured_clock_ghz(torch, fa, ops, w)
-    peak_clk = MXFP4_PEAK_TFLOPS * clk / SPEC_CLOCK_GHZ
+    # the timed kernel back to back on the workload's codes and then on zero codes:
+    # its shader clock in steady state, as in the timed region
+    cvd = None if args.no_clock_vs_data else clock_vs_data(torch, fa, ops, w, out)
+    clk = cvd["workload_codes"]["kernel_clock_ghz"] if cvd else None
+    peak_clk = MXFP4_PEAK_TFLOPS * clk / SPEC_CLOCK_GHZ if clk else None
     n_stream = min(stream_blocks(torch), ops[0].numel() // (256 * 64))  # 64 operand bytes per thread
     stream = sustained_mfma_tflops(torch, fa, ops[2].reshape(-1), ops[0].reshape(-1), blocks=n_stream) \
         if n_stream >= 1 else None
@@ -939,11 +988,12 @@ def main():
         "algorithmic_flops_per_launch": flops,
         "algorithmic_bytes_per_launch": int(w.B * w.H * (3 * w.N * w.d * (0.5 + 1 / 32) + 4 * w.N * w.d)),
         "counters": _counter_view(c_online, fp4_ms),
-        "measured_clock_ghz": round(clk, 3),
-        "peak_at_measured_clock": round(peak_clk, 1),
-        "frac_at_measured_clock": round(tflops / peak_clk, 4),
+        "measured_clock_ghz": round(clk, 3) if clk else None,
+        "peak_at_measured_clock": round(peak_clk, 1) if peak_clk else None,
+        "frac_at_measured_clock": round(tflops / peak_clk, 4) if peak_clk else None,
         "sustained_mfma_stream": round(stream, 1) if stream else None,
         "frac_of_sustained_mfma_stream": round(tflops / stream, 4) if stream else None,
+        "clock_vs_data": cvd,
     }
 
     def route(label, ms, route_flops, inputs=name, **extra):
