@@ -345,6 +345,9 @@ def _sustained_clock(torch, fa, ops, w, out, seconds):
                                                wg_clock=True)["wg_clock"])
             n += 1
         torch.cuda.synchronize()
+    if not recs:   # a window too short for a record in its second half
+        recs.append(fa.debug_directp_mxfp4(*ops, no_rows, softmax_scale=w.softmax_scale, wg_clock=True)["wg_clock"])
+        n += 1
     e.record()
     torch.cuda.synchronize()
     c = torch.cat([r.cpu() for r in recs]).double()
