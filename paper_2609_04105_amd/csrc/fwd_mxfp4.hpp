@@ -44,7 +44,8 @@
 //   lane's 16-byte fragment contiguous): a ring of four tiles filled three
 //   tiles ahead by direct-to-LDS loads.  The key loop is software
 //   pipelined two deep: while the vector ALU maps step g+1 to codes, the
-//   matrix unit runs PV of step g and QK of step g+2.
+//   matrix unit runs PV of step g and QK of step g+2.  The online route at
+//   d = 64 runs one step deep at four waves per SIMD instead.
 // - Workgroups are remapped so that the query tiles of one head run on one XCD
 //   and share its L2 copy of that head's K/V.
 #pragma once
@@ -271,15 +272,23 @@ struct TileCopy {
   }
 };
 
-// Two waves per SIMD, except where the LDS ring allows one workgroup of four
-// waves per CU only (FP8 V tiles with d = 128: 108 KiB), and three for
-// four-wave workgroups with d = 64 and FP4 P/V (40 KiB of LDS each, at most
-// 168 registers).
+// The online route's four-wave workgroups with d = 64 pipeline the key loop one
+// step deep (one S^T buffer, one P operand) to fit 128 registers, so that four
+// workgroups of 40 KiB share a CU's 160 KiB of LDS at four waves per SIMD.
 template <int D, int NW, int VAR>
-constexpr int kMinWaves = (VAR & kPV8) ? ((NW == 4 && D == 128) ? 1 : 2) : ((D == 64 && NW == 4) ? 3 : 2);
+constexpr bool kOneBuffer = D == 64 && NW == 4 && VAR == kVarOnline;
+// Two waves per SIMD, except where the LDS ring allows one workgroup of four
+// waves per CU only (FP8 V tiles with d = 128: 108 KiB), four for the one-buffer
+// form above, and three for the other four-wave workgroups with d = 64 and FP4
+// P/V (40 KiB of LDS each, at most 168 registers).
+template <int D, int NW, int VAR>
+constexpr int kMinWaves = (VAR & kPV8) ? ((NW == 4 && D == 128) ? 1 : 2)
+                                       : (kOneBuffer<D, NW, VAR> ? 4 : ((D == 64 && NW == 4) ? 3 : 2));
+template <int D, int NW, int VAR>
+constexpr int kMaxWaves = kMinWaves<D, NW, VAR> > 2 ? kMinWaves<D, NW, VAR> : 2;
 
 template <int D, int NW, bool DUMP, int EX2, int VAR>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kMinWaves<D, NW, VAR>, kMinWaves<D, NW, VAR> > 2 ? 3 : 2))) void
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kMinWaves<D, NW, VAR>, kMaxWaves<D, NW, VAR>))) void
 fwd_mxfp4_kernel(const KParams p) {
   constexpr bool PV8 = (VAR & kPV8) != 0;  // FP8 (E4M3) P and V payloads
   constexpr bool GUARD = (VAR & 7) == kVarGuard, CAUSAL = (VAR & 7) == kVarCausal;
@@ -614,89 +623,130 @@ fwd_mxfp4_kernel(const KParams p) {
   Copy::arrange(ring(I0{}), tid);
   __syncthreads();
 
-  // Two S^T buffers and two P operands alternate with the step parity.
-  v16f SA[2], SB[2];
-  POp PA, PB;
-  int uA, uB;
-  if constexpr (GUARD) {
-    // Anchor (Alg. 3, steps 1-2): the largest score of the first key tile, which
-    // holds the anchor keys; each lane half has two of its four 32-key blocks.
-    qk(ring(I0{}), std::integral_constant<int, 0>{}, SB);
-    qk(ring(I0{}), std::integral_constant<int, 1>{}, SA);
-    float am = fmaxf(SB[0][0], SB[1][0]);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, SB[0][r]), SB[1][r]);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, SA[0][r]), SA[1][r]);
-    unsigned ma = as_uint(am), mb = ma;
-    swap_halves(ma, mb);
-    {
-#pragma clang fp contract(off)
-      const float Y = fmaxf(as_float(ma), as_float(mb)) * p.c_y;
-      Rref = Y + p.margin;
+  if constexpr (kOneBuffer<D, NW, VAR>) {
+    // One step deep: step g runs PV(g), then QK(g+1) and its code map, which
+    // waits for those products; the other waves of the SIMD fill the wait.  The
+    // tile that QK(g+1) reads first is published in the step before it (the
+    // second step of a tile), by the same waits, barrier and copy as below.
+    v16f S1[2];
+    POp P1;
+    int u1;
+    qk(ring(I0{}), std::integral_constant<int, 0>{}, S1);
+    directp(S1, 0, P1, u1, std::false_type{});
+    auto step1 = [&](auto J_, auto TAIL_, int g) {
+      constexpr int j = decltype(J_)::value;
+      constexpr bool guard = decltype(TAIL_)::value;
+      constexpr int sl = j % 2;
+      using b_cur = std::integral_constant<int, j / 2>;
+      using b_nxt = std::integral_constant<int, j / 2 + 1>;
+      using b_new = std::integral_constant<int, j / 2 + 3>;
+      const int t = g >> 1;
+      pv(ring(b_cur{}), std::integral_constant<int, sl>{}, P1, u1);
+      if constexpr (sl == 1) {
+        vm_wait<kBatch>();  // tile t+1 has landed: only tile t+2's loads may be in flight
+        if (!guard || t + 1 < ntiles) Copy::arrange(ring(b_nxt{}), tid);
+        __syncthreads();
+        copy.issue(ring(b_new{}), (t + 3) * kBN);
+      }
+      if (!guard || g + 1 < nsteps) {
+        if constexpr (sl == 0) qk(ring(b_cur{}), std::integral_constant<int, 1>{}, S1);
+        else qk(ring(b_nxt{}), std::integral_constant<int, 0>{}, S1);
+        directp(S1, g + 1, P1, u1, std::false_type{});
+      }
+    };
+    int g0 = 0;
+    for (; g0 + 8 <= nsteps - 2; g0 += 8) {
+      static_for<8>([&](auto J_) { step1(J_, std::false_type{}, g0 + decltype(J_)::value); });
     }
-    directp(SB, 0, PA, uA, std::false_type{});
+    static_for<10>([&](auto J_) {  // tail: fewer than 10 steps remain
+      const int g = g0 + decltype(J_)::value;
+      if (g < nsteps) step1(J_, std::true_type{}, g);
+    });
   } else {
-    qk(ring(I0{}), std::integral_constant<int, 0>{}, SA);
-    if constexpr (CAUSAL) causal_mask(SA, 0);
-    directp(SA, 0, PA, uA, std::false_type{});
-    qk(ring(I0{}), std::integral_constant<int, 1>{}, SA);
+    // Two S^T buffers and two P operands alternate with the step parity.
+    v16f SA[2], SB[2];
+    POp PA, PB;
+    int uA, uB;
+    if constexpr (GUARD) {
+      // Anchor (Alg. 3, steps 1-2): the largest score of the first key tile, which
+      // holds the anchor keys; each lane half has two of its four 32-key blocks.
+      qk(ring(I0{}), std::integral_constant<int, 0>{}, SB);
+      qk(ring(I0{}), std::integral_constant<int, 1>{}, SA);
+      float am = fmaxf(SB[0][0], SB[1][0]);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, SB[0][r]), SB[1][r]);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, SA[0][r]), SA[1][r]);
+      unsigned ma = as_uint(am), mb = ma;
+      swap_halves(ma, mb);
+      {
+#pragma clang fp contract(off)
+        const float Y = fmaxf(as_float(ma), as_float(mb)) * p.c_y;
+        Rref = Y + p.margin;
+      }
+      directp(SB, 0, PA, uA, std::false_type{});
+    } else {
+      qk(ring(I0{}), std::integral_constant<int, 0>{}, SA);
+      if constexpr (CAUSAL) causal_mask(SA, 0);
+      directp(SA, 0, PA, uA, std::false_type{});
+      qk(ring(I0{}), std::integral_constant<int, 1>{}, SA);
+    }
+
+    // One step of the pipeline; j is the step's position in its group of eight.
+    // TAIL: the tail group, where QK, Direct-P or the step itself may not exist.
+    auto step = [&](auto J_, auto TAIL_, int g) {
+      constexpr int j = decltype(J_)::value;
+      constexpr bool guard = decltype(TAIL_)::value;
+      constexpr int sl = j % 2;                 // step within its tile
+      using b_cur = std::integral_constant<int, j / 2>;  // ring stage of tile t
+      using b_nxt = std::integral_constant<int, j / 2 + 1>;
+      using b_new = std::integral_constant<int, j / 2 + 3>;
+      auto& S_in = (sl == 0) ? SA : SB;   // S^T of step g+1
+      auto& S_out = (sl == 0) ? SB : SA;  // S^T of step g+2
+      auto& P_cur = (sl == 0) ? PA : PB;  // P of step g
+      auto& u_cur = (sl == 0) ? uA : uB;
+      auto& P_nxt = (sl == 0) ? PB : PA;  // P of step g+1
+      auto& u_nxt = (sl == 0) ? uB : uA;
+      const int t = g >> 1;
+      // PV of step g and Direct-P of step g+1 read nothing the barrier publishes,
+      // so they come first: the matrix unit has PV's products in hand while the
+      // waves meet at the barrier.
+      pv(ring(b_cur{}), std::integral_constant<int, sl>{}, P_cur, u_cur);
+      if (!guard || g + 1 < nsteps) {
+        // masked steps all fall in the tail group (see the loop bound below)
+        if constexpr (CAUSAL && guard) causal_mask(S_in, g + 1);
+        directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
+      }
+      if constexpr (sl == 0) {
+        vm_wait<kBatch>();  // tile t+1 has landed: only tile t+2's loads may be in flight
+        if (!guard || t + 1 < ntiles) Copy::arrange(ring(b_nxt{}), tid);
+        __syncthreads();
+        copy.issue(ring(b_new{}), (t + 3) * kBN);
+      }
+      if (!guard || g + 2 < nsteps) {
+        qk(ring(b_nxt{}), std::integral_constant<int, sl>{}, S_out);
+        // Issue QK of step g+2 in this step (it would otherwise sink next to its
+        // consumer in step g+1 and serialise with the code map); emits nothing.
+        asm volatile("" ::"v"(S_out[0]), "v"(S_out[1]));
+      }
+    };
+
+
+    // The unrolled loop stops kLeft steps before the end, so that the tail group
+    // holds every step that may lack QK or Direct-P work and, with the causal
+    // mask, every step whose keys reach past a query of the tile: Direct-P of
+    // step g' >= nsteps - BM / 64 runs in step g' - 1.
+    constexpr int kLeft = CAUSAL ? BM / 64 + 1 : 2;
+    int g0 = 0;
+    for (; g0 + 8 <= nsteps - kLeft; g0 += 8) {
+      static_for<8>([&](auto J_) { step(J_, std::false_type{}, g0 + decltype(J_)::value); });
+    }
+    // tail: fewer than 8 + kLeft steps remain
+    static_for<8 + kLeft>([&](auto J_) {
+      const int g = g0 + decltype(J_)::value;
+      if (g < nsteps) step(J_, std::true_type{}, g);
+    });
   }
-
-  // One step of the pipeline; j is the step's position in its group of eight.
-  // TAIL: the tail group, where QK, Direct-P or the step itself may not exist.
-  auto step = [&](auto J_, auto TAIL_, int g) {
-    constexpr int j = decltype(J_)::value;
-    constexpr bool guard = decltype(TAIL_)::value;
-    constexpr int sl = j % 2;                 // step within its tile
-    using b_cur = std::integral_constant<int, j / 2>;  // ring stage of tile t
-    using b_nxt = std::integral_constant<int, j / 2 + 1>;
-    using b_new = std::integral_constant<int, j / 2 + 3>;
-    auto& S_in = (sl == 0) ? SA : SB;   // S^T of step g+1
-    auto& S_out = (sl == 0) ? SB : SA;  // S^T of step g+2
-    auto& P_cur = (sl == 0) ? PA : PB;  // P of step g
-    auto& u_cur = (sl == 0) ? uA : uB;
-    auto& P_nxt = (sl == 0) ? PB : PA;  // P of step g+1
-    auto& u_nxt = (sl == 0) ? uB : uA;
-    const int t = g >> 1;
-    // PV of step g and Direct-P of step g+1 read nothing the barrier publishes,
-    // so they come first: the matrix unit has PV's products in hand while the
-    // waves meet at the barrier.
-    pv(ring(b_cur{}), std::integral_constant<int, sl>{}, P_cur, u_cur);
-    if (!guard || g + 1 < nsteps) {
-      // masked steps all fall in the tail group (see the loop bound below)
-      if constexpr (CAUSAL && guard) causal_mask(S_in, g + 1);
-      directp(S_in, g + 1, P_nxt, u_nxt, std::bool_constant<!guard>{});
-    }
-    if constexpr (sl == 0) {
-      vm_wait<kBatch>();  // tile t+1 has landed: only tile t+2's loads may be in flight
-      if (!guard || t + 1 < ntiles) Copy::arrange(ring(b_nxt{}), tid);
-      __syncthreads();
-      copy.issue(ring(b_new{}), (t + 3) * kBN);
-    }
-    if (!guard || g + 2 < nsteps) {
-      qk(ring(b_nxt{}), std::integral_constant<int, sl>{}, S_out);
-      // Issue QK of step g+2 in this step (it would otherwise sink next to its
-      // consumer in step g+1 and serialise with the code map); emits nothing.
-      asm volatile("" ::"v"(S_out[0]), "v"(S_out[1]));
-    }
-  };
-
-
-  // The unrolled loop stops kLeft steps before the end, so that the tail group
-  // holds every step that may lack QK or Direct-P work and, with the causal
-  // mask, every step whose keys reach past a query of the tile: Direct-P of
-  // step g' >= nsteps - BM / 64 runs in step g' - 1.
-  constexpr int kLeft = CAUSAL ? BM / 64 + 1 : 2;
-  int g0 = 0;
-  for (; g0 + 8 <= nsteps - kLeft; g0 += 8) {
-    static_for<8>([&](auto J_) { step(J_, std::false_type{}, g0 + decltype(J_)::value); });
-  }
-  // tail: fewer than 8 + kLeft steps remain
-  static_for<8 + kLeft>([&](auto J_) {
-    const int g = g0 + decltype(J_)::value;
-    if (g < nsteps) step(J_, std::true_type{}, g);
-  });
   vm_wait<0>();  // no copy may still be landing in LDS when the workgroup ends
 
   // Epilogue: O = acc / (6 D).  The denominator sits in register 0 of the lower half.
