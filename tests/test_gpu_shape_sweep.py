@@ -26,7 +26,7 @@ SHAPES = [  # B, H, N, d
     (2, 40, 1536, 128),    # 480: last round 224 (eight waves)
     (1, 1290, 256, 128),   # 1290: six rounds (eight waves)
     (3, 7, 1664, 128),     # N = 13 x 128: four-wave launch
-    (2, 3, 4224, 64),      # N = 33 x 128, d = 64 (three waves per SIMD)
+    (2, 3, 4224, 64),      # N = 33 x 128, d = 64 (four waves per SIMD; three causal or guarded)
     (1, 3, 12288, 128),    # 144 workgroups: fewer than the CUs
     (1, 6, 8320, 64),      # N = 65 x 128
     (1, 1, 128, 128),      # one tile
@@ -57,7 +57,7 @@ def test_every_route_at_launch_boundaries(B, H, N, d):
 @pytest.mark.parametrize("H,N,d", [(24, 32768, 128), (64, 32768, 64)])
 def test_paper_largest_shapes_sampled_rows(H, N, d):
     """The largest shapes of the paper's D128 and D64 tables (B1), in the launch the
-    benchmark times (eight-wave workgroups at d = 128; 128-query workgroups at three
+    benchmark times (eight-wave workgroups at d = 128; 128-query workgroups at four
     waves per SIMD at d = 64): bf16 N(0,1) inputs drawn on the GPU, 24 rows from six
     heads (the first and last of the sequence among them) against the oracle."""
     import paper_2609_04105_amd as fa
