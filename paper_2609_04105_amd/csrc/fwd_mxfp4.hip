@@ -104,15 +104,14 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   // sooner (B1 N4096 d128: +9 % at H24, +10 % at H36, +4 % at H40, +3 % at H72;
   // -2 % with ten rounds at H64 N9472, and a full last round favours eight waves
   // by 4-7 %).  The FP8 route and the causal forward keep eight waves.
-  // With d = 64 (FP4 P/V) every launch takes four-wave workgroups: four per CU for
-  // the online route (one-step pipeline, four waves per SIMD; +1-4 % over three
-  // on the paper's D64 shapes), three for the guarded and causal routes (B1 d64,
-  // three against two waves per SIMD: +7 % at H24 and H64 N32768, +9-10 % at H24
-  // and H64 N4096, equal on grids that leave CUs idle).
+  // With d = 64 (FP4 P/V) every launch takes four-wave workgroups, four per CU
+  // (one-step pipeline, four waves per SIMD; against three waves with two score
+  // buffers, +1-4 % on the paper's D64 shapes, which in turn gained 7-10 % over
+  // two waves).
   const int64_t wide_wgs = a.N % 256 == 0 ? (int64_t)(a.N / 256) * bh : 0;
   const int64_t last_round = wide_wgs % 256;
   const bool tail = wide_wgs > 256 && wide_wgs <= 5 * 256 && last_round != 0 && last_round <= 128;
-  const bool three_waves = a.d == 64 && !a.pv_fp8;  // the 128-query d = 64 launch (three or four waves per SIMD)
+  const bool three_waves = a.d == 64 && !a.pv_fp8;  // the 128-query d = 64 launch (four waves per SIMD)
   const bool wide = wide_wgs >= 256 && !(tail && !a.pv_fp8 && !a.causal) && !three_waves;
   const int BM = wide ? 256 : 128;
   kp.n_qtiles = a.N / BM;

@@ -44,8 +44,8 @@
 //   lane's 16-byte fragment contiguous): a ring of four tiles filled three
 //   tiles ahead by direct-to-LDS loads.  The key loop is software
 //   pipelined two deep: while the vector ALU maps step g+1 to codes, the
-//   matrix unit runs PV of step g and QK of step g+2.  The online route at
-//   d = 64 runs one step deep at four waves per SIMD instead.
+//   matrix unit runs PV of step g and QK of step g+2.  With d = 64 and FP4 P/V
+//   the loop runs one step deep at four waves per SIMD instead.
 // - Workgroups are remapped so that the query tiles of one head run on one XCD
 //   and share its L2 copy of that head's K/V.
 #pragma once
@@ -272,15 +272,14 @@ struct TileCopy {
   }
 };
 
-// The online route's four-wave workgroups with d = 64 pipeline the key loop one
+// The FP4 P/V routes' four-wave workgroups with d = 64 pipeline the key loop one
 // step deep (one S^T buffer, one P operand) to fit 128 registers, so that four
 // workgroups of 40 KiB share a CU's 160 KiB of LDS at four waves per SIMD.
 template <int D, int NW, int VAR>
-constexpr bool kOneBuffer = D == 64 && NW == 4 && VAR == kVarOnline;
+constexpr bool kOneBuffer = D == 64 && NW == 4 && (VAR & kPV8) == 0;
 // Two waves per SIMD, except where the LDS ring allows one workgroup of four
-// waves per CU only (FP8 V tiles with d = 128: 108 KiB), four for the one-buffer
-// form above, and three for the other four-wave workgroups with d = 64 and FP4
-// P/V (40 KiB of LDS each, at most 168 registers).
+// waves per CU only (FP8 V tiles with d = 128: 108 KiB), and four for the
+// one-buffer form above.
 template <int D, int NW, int VAR>
 constexpr int kMinWaves = (VAR & kPV8) ? ((NW == 4 && D == 128) ? 1 : 2)
                                        : (kOneBuffer<D, NW, VAR> ? 4 : ((D == 64 && NW == 4) ? 3 : 2));
@@ -631,7 +630,26 @@ fwd_mxfp4_kernel(const KParams p) {
     v16f S1[2];
     POp P1;
     int u1;
-    qk(ring(I0{}), std::integral_constant<int, 0>{}, S1);
+    if constexpr (GUARD) {
+      // Anchor (Alg. 3, steps 1-2) over both steps of the first key tile, one step
+      // at a time; the buffer ends with step 0's scores for its code map.
+      float am = -__builtin_inff();
+      static_for<2>([&](auto T_) {
+        qk(ring(I0{}), std::integral_constant<int, 1 - decltype(T_)::value>{}, S1);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) am = fmaxf(fmaxf(am, S1[0][r]), S1[1][r]);
+      });
+      unsigned ma = as_uint(am), mb = ma;
+      swap_halves(ma, mb);
+      {
+#pragma clang fp contract(off)
+        const float Y = fmaxf(as_float(ma), as_float(mb)) * p.c_y;
+        Rref = Y + p.margin;
+      }
+    } else {
+      qk(ring(I0{}), std::integral_constant<int, 0>{}, S1);
+    }
+    if constexpr (CAUSAL) causal_mask(S1, 0);
     directp(S1, 0, P1, u1, std::false_type{});
     auto step1 = [&](auto J_, auto TAIL_, int g) {
       constexpr int j = decltype(J_)::value;
@@ -651,14 +669,19 @@ fwd_mxfp4_kernel(const KParams p) {
       if (!guard || g + 1 < nsteps) {
         if constexpr (sl == 0) qk(ring(b_cur{}), std::integral_constant<int, 1>{}, S1);
         else qk(ring(b_nxt{}), std::integral_constant<int, 0>{}, S1);
+        // masked steps all fall in the tail group (see the loop bound below)
+        if constexpr (CAUSAL && guard) causal_mask(S1, g + 1);
         directp(S1, g + 1, P1, u1, std::false_type{});
       }
     };
+    // As below: the tail group holds every step whose keys reach past a query of
+    // the tile (Direct-P of step g' >= nsteps - BM / 64 runs in step g' - 1).
+    constexpr int kLeft1 = CAUSAL ? BM / 64 + 1 : 2;
     int g0 = 0;
-    for (; g0 + 8 <= nsteps - 2; g0 += 8) {
+    for (; g0 + 8 <= nsteps - kLeft1; g0 += 8) {
       static_for<8>([&](auto J_) { step1(J_, std::false_type{}, g0 + decltype(J_)::value); });
     }
-    static_for<10>([&](auto J_) {  // tail: fewer than 10 steps remain
+    static_for<8 + kLeft1>([&](auto J_) {  // tail: fewer than 8 + kLeft1 steps remain
       const int g = g0 + decltype(J_)::value;
       if (g < nsteps) step1(J_, std::true_type{}, g);
     });

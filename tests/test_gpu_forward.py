@@ -197,8 +197,7 @@ def _check_byte_operands(fa, ops_cpu, rows, label, causal=False, guard=None, pv_
 def test_longest_sequence_sampled_rows(fa, d, causal):
     """N = 2^22 keys, the largest the entry point accepts: every byte offset within
     the head near its 32-bit limit, 32768 key tiles per workgroup; d = 64 takes
-    128-query workgroups (four waves per SIMD, one-step pipeline, on the plain route;
-    three on the causal one).  Rows: the first and last of the
+    128-query workgroups at four waves per SIMD (one-step pipeline).  Rows: the first and last of the
     sequence, of a query tile and of a workgroup, and random ones."""
     N = 1 << 22
     ops_cpu = workloads.random_mxfp4_operands(1, 1, N, d, seed=22 + d)

@@ -26,7 +26,7 @@ SHAPES = [  # B, H, N, d
     (2, 40, 1536, 128),    # 480: last round 224 (eight waves)
     (1, 1290, 256, 128),   # 1290: six rounds (eight waves)
     (3, 7, 1664, 128),     # N = 13 x 128: four-wave launch
-    (2, 3, 4224, 64),      # N = 33 x 128, d = 64 (four waves per SIMD; three causal or guarded)
+    (2, 3, 4224, 64),      # N = 33 x 128, d = 64 (four waves per SIMD)
     (1, 3, 12288, 128),    # 144 workgroups: fewer than the CUs
     (1, 6, 8320, 64),      # N = 65 x 128
     (1, 1, 128, 128),      # one tile
