@@ -104,15 +104,20 @@ hipError_t launch_forward_mxfp4(const DirectPArgs& a, hipStream_t stream) {
   // sooner (B1 N4096 d128: +9 % at H24, +10 % at H36, +4 % at H40, +3 % at H72;
   // -2 % with ten rounds at H64 N9472, and a full last round favours eight waves
   // by 4-7 %).  The FP8 route and the causal forward keep eight waves.
-  // With d = 64 (FP4 P/V) every launch takes four-wave workgroups, four per CU
-  // (one-step pipeline, four waves per SIMD; against three waves with two score
-  // buffers, +1-4 % on the paper's D64 shapes, which in turn gained 7-10 % over
-  // two waves).
+  // With d = 64 (FP4 P/V) the kernel runs at four waves per SIMD (one-step
+  // pipeline; against three waves with two score buffers, +1-4 % on the paper's
+  // D64 shapes, which in turn gained 7-10 % over two waves).  Eight-wave
+  // workgroups, two per CU, when the eight-wave grid is a whole number of half
+  // rounds (a multiple of 256 workgroups: +4-8 % at B1 N4096 H16-H128 and on the
+  // paper's large shapes) and, for the causal forward, at least 3072 of them
+  // (+2.5-5.7 %; -1 to -2 % at 1024-2048); otherwise four-wave workgroups, four
+  // per CU (eight waves lost 6-15 % where the last half round is partly filled).
   const int64_t wide_wgs = a.N % 256 == 0 ? (int64_t)(a.N / 256) * bh : 0;
   const int64_t last_round = wide_wgs % 256;
   const bool tail = wide_wgs > 256 && wide_wgs <= 5 * 256 && last_round != 0 && last_round <= 128;
-  const bool three_waves = a.d == 64 && !a.pv_fp8;  // the 128-query d = 64 launch (four waves per SIMD)
-  const bool wide = wide_wgs >= 256 && !(tail && !a.pv_fp8 && !a.causal) && !three_waves;
+  const bool d64 = a.d == 64 && !a.pv_fp8;
+  const bool d64_wide = wide_wgs >= 256 && last_round == 0 && (!a.causal || wide_wgs >= 3072);
+  const bool wide = d64 ? d64_wide : (wide_wgs >= 256 && !(tail && !a.pv_fp8 && !a.causal));
   const int BM = wide ? 256 : 128;
   kp.n_qtiles = a.N / BM;
   kp.total = kp.n_qtiles * bh;

@@ -272,11 +272,11 @@ struct TileCopy {
   }
 };
 
-// The FP4 P/V routes' four-wave workgroups with d = 64 pipeline the key loop one
-// step deep (one S^T buffer, one P operand) to fit 128 registers, so that four
-// workgroups of 40 KiB share a CU's 160 KiB of LDS at four waves per SIMD.
+// The FP4 P/V routes with d = 64 pipeline the key loop one step deep (one S^T
+// buffer, one P operand) to fit 128 registers: four waves per SIMD, i.e. four
+// four-wave or two eight-wave workgroups of 40 KiB LDS per CU.
 template <int D, int NW, int VAR>
-constexpr bool kOneBuffer = D == 64 && NW == 4 && (VAR & kPV8) == 0;
+constexpr bool kOneBuffer = D == 64 && (VAR & kPV8) == 0;
 // Two waves per SIMD, except where the LDS ring allows one workgroup of four
 // waves per CU only (FP8 V tiles with d = 128: 108 KiB), and four for the
 // one-buffer form above.

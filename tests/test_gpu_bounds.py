@@ -39,7 +39,7 @@ def _p(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
-SHAPES = [(1, 3, 384, 128), (2, 5, 640, 64), (1, 1, 128, 64), (1, 24, 4096, 128)]
+SHAPES = [(1, 3, 384, 128), (2, 5, 640, 64), (1, 1, 128, 64), (1, 24, 4096, 128), (1, 16, 4096, 64)]
 
 
 @pytest.mark.parametrize("B,H,N,d", SHAPES)

@@ -7,7 +7,8 @@ a round and a last round of 64 (both take the four-wave tail launch on the
 plain route, eight waves on the causal and FP8 routes); a last round of 224
 (eight waves); more than five rounds; sequence lengths that are odd multiples
 of 128 (four-wave launch), with batch > 1; the longest sequence below which
-the grid leaves CUs idle; and the smallest problem.  Rows: the first and last
+the grid leaves CUs idle; d = 64 grids of eight-wave workgroups (two per CU), the causal
+route's among them; and the smallest problem.  Rows: the first and last
 of the tensor and of a head, and seeded random ones.  Also the largest shapes of
 the paper's D128 and D64 tables, which the benchmark times."""
 import numpy as np
@@ -29,6 +30,8 @@ SHAPES = [  # B, H, N, d
     (2, 3, 4224, 64),      # N = 33 x 128, d = 64 (four waves per SIMD)
     (1, 3, 12288, 128),    # 144 workgroups: fewer than the CUs
     (1, 6, 8320, 64),      # N = 65 x 128
+    (1, 16, 4096, 64),     # d = 64, 256 eight-wave workgroups: two per CU (causal: four-wave)
+    (1, 768, 1024, 64),    # d = 64, 3072 eight-wave workgroups: the causal route takes them too
     (1, 1, 128, 128),      # one tile
 ]
 
